@@ -1,0 +1,221 @@
+// RDF2vec random-walk corpus extraction: CPU oracle.
+//
+// TEST INFRASTRUCTURE, NOT PRODUCT CODE. This file is a plain, slow,
+// single-threaded statement of what the GPU library computes. Only the test
+// suite, the smoke check and the CPU-baseline leg of the benchmark load it; the
+// GPU library never calls, links or includes it, and it includes nothing from
+// the GPU library. It has no blocking, no fusion and no reordering beyond the
+// definitions below, so that each step can be checked against its source by eye.
+//
+// What it computes (gpuRDF2vec, Boeckling & Paulheim, arXiv 2508.01073):
+//  * Sec. 2: a random walk is the iterative random choice of the next hop.
+//  * Sec. 3.1: entities and predicates are tokenised to integer ids, walks are
+//    emitted as entity/predicate (triple-based) sequences, and a walk that ends
+//    before the maximum depth is padded with -1.
+//  * Sec. 3.3: the walk parameters are the start entities, the depth, the
+//    number of walks per entity and a random seed. The paper does not fix the
+//    generator; this library fixes it to Philox4x32-10 (Salmon, Moraes, Dror &
+//    Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC'11), keyed on the
+//    seed and counted on (walk id, hop / 4), with the next out-edge chosen as
+//    floor(u * deg / 2^32) over the out-edge records of the current entity.
+//
+// Readings where the paper is silent (each is listed in the design notes):
+//  * CSR rows keep the input order of the triples (a stable sort by subject).
+//  * Depth counts hops; a walk row holds 2*depth+1 tokens.
+//  * Hops are numbered from 0; walk w starts at start[w / walks_per_node].
+//  * Entity token = entity id; predicate token = num_entities + predicate id.
+//  * An entity with no out-edge is a sink: the walk stops there.
+//  * Duplicate triples and self-loops are kept and followed like any edge.
+//
+// parity pinned: Philox against rocRAND's host-callable Philox4x32-10, the edge
+// index against its closed form, the CSR against std::stable_sort / numpy's
+// stable argsort, and the walks against chain, sink, brute-force-enumeration and
+// chi-square uniformity tests (see tests/test_oracle_pins.py).
+
+#include <cstdint>
+#include <cstddef>
+#include <vector>
+
+namespace {
+
+// Status codes: the same numbering as the library's public header, restated
+// here so that the two share no file.
+enum : int {
+  REF_OK = 0,
+  REF_ERR_INVALID_ARGUMENT = 1,
+  REF_ERR_ID_OUT_OF_RANGE = 2,
+  REF_ERR_TOO_LARGE = 3,
+};
+
+constexpr int64_t kInt32Limit = int64_t(1) << 31;
+constexpr int kMaxDepth = 64;
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon et al., SC'11, Sec. 4 "Philox"): a counter-based
+// generator. Each of ten rounds multiplies counter words 0 and 2 by the two
+// Philox multipliers, forming 32x32->64-bit products (hi, lo); the new counter
+// is (hi of product 2 ^ c1 ^ k0, lo of product 2, hi of product 0 ^ c3 ^ k1,
+// lo of product 0). Between rounds the key is advanced by the two Weyl
+// constants (the golden ratio and sqrt(3)-1 scaled to 32 bits), mod 2^32.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kPhiloxM0 = 0xD2511F53u;
+constexpr uint32_t kPhiloxM1 = 0xCD9E8D57u;
+constexpr uint32_t kPhiloxW0 = 0x9E3779B9u;
+constexpr uint32_t kPhiloxW1 = 0xBB67AE85u;
+
+void philox4x32_10(const uint32_t counter[4], const uint32_t key[2], uint32_t out[4]) {
+  uint32_t c0 = counter[0], c1 = counter[1], c2 = counter[2], c3 = counter[3];
+  uint32_t k0 = key[0], k1 = key[1];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) {
+      k0 += kPhiloxW0;
+      k1 += kPhiloxW1;
+    }
+    const uint64_t prod0 = uint64_t(kPhiloxM0) * uint64_t(c0);
+    const uint64_t prod1 = uint64_t(kPhiloxM1) * uint64_t(c2);
+    const uint32_t hi0 = uint32_t(prod0 >> 32), lo0 = uint32_t(prod0);
+    const uint32_t hi1 = uint32_t(prod1 >> 32), lo1 = uint32_t(prod1);
+    const uint32_t n0 = hi1 ^ c1 ^ k0;
+    const uint32_t n1 = lo1;
+    const uint32_t n2 = hi0 ^ c3 ^ k1;
+    const uint32_t n3 = lo0;
+    c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+  }
+  out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+// The random word for hop h of walk w: block number h / 4 of the walk's stream
+// (walk id in the high counter half), word h mod 4 of that block.
+uint32_t philox_word(uint64_t seed, uint64_t walk, uint64_t hop) {
+  const uint64_t block = hop >> 2;
+  const uint32_t counter[4] = {uint32_t(block), uint32_t(block >> 32),
+                               uint32_t(walk), uint32_t(walk >> 32)};
+  const uint32_t key[2] = {uint32_t(seed), uint32_t(seed >> 32)};
+  uint32_t out[4];
+  philox4x32_10(counter, key, out);
+  return out[hop & 3];
+}
+
+// Uniform choice of one of deg out-edge records from a 32-bit word:
+// floor(u * deg / 2^32), always in [0, deg) for deg >= 1.
+uint32_t edge_index(uint32_t u, uint32_t deg) {
+  return uint32_t((uint64_t(u) * uint64_t(deg)) >> 32);
+}
+
+}  // namespace
+
+extern "C" {
+
+void rdf2v_ref_philox4x32_10(const uint32_t counter[4], const uint32_t key[2], uint32_t out[4]) {
+  philox4x32_10(counter, key, out);
+}
+
+uint32_t rdf2v_ref_philox_word(uint64_t seed, uint64_t walk, uint64_t hop) {
+  return philox_word(seed, walk, hop);
+}
+
+uint32_t rdf2v_ref_edge_index(uint32_t u, uint32_t deg) { return edge_index(u, deg); }
+
+// Subject-indexed CSR of (predicate, object) out-edge records (Sec. 3.1: the
+// triples are loaded as a graph whose traversal yields the walks).
+//   row_ptr[V+1]: row_ptr[v] .. row_ptr[v+1] are the out-edges of entity v.
+//   edges[T][2]:  (predicate, object) records; inside a row, input order.
+int rdf2v_ref_build_csr(const int32_t *subj, const int32_t *pred, const int32_t *obj,
+                        int64_t num_triples, int32_t num_entities, int32_t num_predicates,
+                        int32_t *row_ptr, int32_t *edges) {
+  if (num_triples < 0 || num_entities < 0 || num_predicates < 0) return REF_ERR_INVALID_ARGUMENT;
+  if (row_ptr == nullptr) return REF_ERR_INVALID_ARGUMENT;
+  if (num_triples > 0 && (subj == nullptr || pred == nullptr || obj == nullptr || edges == nullptr))
+    return REF_ERR_INVALID_ARGUMENT;
+  if (num_triples >= kInt32Limit) return REF_ERR_TOO_LARGE;
+  if (int64_t(num_entities) + int64_t(num_predicates) >= kInt32Limit) return REF_ERR_TOO_LARGE;
+
+  for (int64_t t = 0; t < num_triples; ++t) {
+    if (subj[t] < 0 || subj[t] >= num_entities) return REF_ERR_ID_OUT_OF_RANGE;
+    if (obj[t] < 0 || obj[t] >= num_entities) return REF_ERR_ID_OUT_OF_RANGE;
+    if (pred[t] < 0 || pred[t] >= num_predicates) return REF_ERR_ID_OUT_OF_RANGE;
+  }
+
+  // Out-degree of every entity.
+  std::vector<int64_t> degree(size_t(num_entities), 0);
+  for (int64_t t = 0; t < num_triples; ++t) degree[size_t(subj[t])] += 1;
+
+  // Row offsets: exclusive prefix sum of the degrees.
+  row_ptr[0] = 0;
+  for (int32_t v = 0; v < num_entities; ++v)
+    row_ptr[v + 1] = int32_t(int64_t(row_ptr[v]) + degree[size_t(v)]);
+
+  // Place each triple at the next free slot of its subject's row, visiting the
+  // triples in input order: this keeps input order inside every row.
+  std::vector<int64_t> cursor(size_t(num_entities), 0);
+  for (int32_t v = 0; v < num_entities; ++v) cursor[size_t(v)] = row_ptr[v];
+  for (int64_t t = 0; t < num_triples; ++t) {
+    const int64_t slot = cursor[size_t(subj[t])]++;
+    edges[2 * slot + 0] = pred[t];
+    edges[2 * slot + 1] = obj[t];
+  }
+  return REF_OK;
+}
+
+// Entities with at least one out-edge, ascending: the default start set (the
+// paper starts walks from every entity when no start list is given, Sec. 3.3;
+// a sink start would only yield a one-token walk).
+int64_t rdf2v_ref_nonsink_starts(const int32_t *row_ptr, int32_t num_entities, int32_t *starts_out) {
+  int64_t n = 0;
+  for (int32_t v = 0; v < num_entities; ++v)
+    if (row_ptr[v + 1] > row_ptr[v]) starts_out[n++] = v;
+  return n;
+}
+
+// Walks w in [walk_begin, walk_begin + walk_count) of the corpus with
+// num_start * walks_per_node walks. Row r = w - walk_begin of the outputs:
+//   tokens[r][0 .. 2*depth]: e0, V+p0, e1, V+p1, e2, ...; -1 after the end.
+//   len[r]: number of valid tokens = 2 * hops + 1.
+int rdf2v_ref_random_walks(const int32_t *row_ptr, const int32_t *edges, int32_t num_entities,
+                           int32_t num_predicates, int64_t num_edges, const int32_t *start_nodes,
+                           int64_t num_start, int32_t walks_per_node, int32_t depth, uint64_t seed,
+                           int64_t walk_begin, int64_t walk_count, int32_t *tokens, int32_t *len) {
+  if (num_entities < 0 || num_predicates < 0 || num_edges < 0 || num_start < 0) return REF_ERR_INVALID_ARGUMENT;
+  if (walks_per_node < 0 || depth < 0 || depth > kMaxDepth) return REF_ERR_INVALID_ARGUMENT;
+  if (walk_begin < 0 || walk_count < 0) return REF_ERR_INVALID_ARGUMENT;
+  if (num_edges >= kInt32Limit) return REF_ERR_TOO_LARGE;
+  if (int64_t(num_entities) + int64_t(num_predicates) >= kInt32Limit) return REF_ERR_TOO_LARGE;
+  const int64_t num_walks = num_start * int64_t(walks_per_node);  // callers keep this in range
+  if (walk_begin > num_walks || walk_count > num_walks - walk_begin) return REF_ERR_INVALID_ARGUMENT;
+  if (walk_count == 0) return REF_OK;
+  if (row_ptr == nullptr || start_nodes == nullptr || tokens == nullptr || len == nullptr)
+    return REF_ERR_INVALID_ARGUMENT;
+
+  const int64_t width = 2 * int64_t(depth) + 1;
+  int status = REF_OK;
+  for (int64_t r = 0; r < walk_count; ++r) {
+    const int64_t w = walk_begin + r;
+    int32_t *row = tokens + r * width;
+    int32_t e = start_nodes[w / walks_per_node];
+    row[0] = e;
+    int64_t n = 1;
+    if (e < 0 || e >= num_entities) status = REF_ERR_ID_OUT_OF_RANGE;
+    for (int32_t h = 0; h < depth && status == REF_OK; ++h) {
+      const int64_t lo = row_ptr[e];
+      const int64_t hi = row_ptr[e + 1];
+      if (lo < 0 || hi < lo || hi > num_edges) { status = REF_ERR_ID_OUT_OF_RANGE; break; }
+      const int64_t degree = hi - lo;
+      if (degree == 0) break;  // sink: the walk ends here
+      const uint32_t u = philox_word(seed, uint64_t(w), uint64_t(h));
+      const int64_t k = edge_index(u, uint32_t(degree));
+      const int32_t p = edges[2 * (lo + k) + 0];
+      const int32_t x = edges[2 * (lo + k) + 1];
+      if (p < 0 || p >= num_predicates || x < 0 || x >= num_entities) { status = REF_ERR_ID_OUT_OF_RANGE; break; }
+      row[2 * h + 1] = num_entities + p;
+      row[2 * h + 2] = x;
+      n += 2;
+      e = x;
+    }
+    for (int64_t j = n; j < width; ++j) row[j] = -1;
+    len[r] = int32_t(n);
+    if (status != REF_OK) return status;
+  }
+  return REF_OK;
+}
+
+}  // extern "C"
