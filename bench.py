@@ -1,0 +1,253 @@
+#!/usr/bin/env python3
+"""Benchmark: RDF2vec random-walk corpus extraction on one MI355X.
+
+One step is one pass of the whole path over inputs already resident in HBM:
+rdf2v_build_csr (triples -> CSR), rdf2v_nonsink_starts (start set) and
+rdf2v_random_walks (every walk of every start entity, one launch). The default
+workload is the power-law graph with 1M entities, 200 predicates and 20M
+triples, depth 8, 50 walks per start entity (about 48.9M walks).
+
+Prints ONE JSON line. `value` is valid walk tokens per second over whole steps;
+`roofline` rates the walk kernel (the dominant kernel) by its useful bytes per
+launch over its average launch time, measured with HIP events on the stream
+the kernels run on; `cpu_baseline` times the CPU oracle on a bounded sample.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "walk tokens/sec on 1 MI355X + achieved HBM GB/s fraction of peak"
+HBM_PEAK_GBS = 8000.0
+PMC_FILE = os.path.join(ROOT, "profiles", "walk_kernel_pmc.json")
+WALK_SOURCES = [os.path.join(ROOT, "paper_2508_01073_amd", "csrc", f)
+                for f in ("random_walk.hip", "common.hpp", "launch.hpp")]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in WALK_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def useful_bytes(lens, depth: int, num_start: int) -> tuple[int, int, int]:
+    """(useful bytes, hops, valid tokens) of one walk launch.
+
+    Gathered: 16 B per hop (the row_ptr pair and one (predicate, object) record),
+    8 B more for a walk that stops at a sink (the row_ptr pair that shows it), and
+    4 B per start id. Written: the padded token row (4 * (2*depth+1) B) and the
+    length (4 B) of every walk."""
+    import torch
+    width = 2 * depth + 1
+    ln = lens.to(torch.int64)
+    tokens = int(ln.sum().item())
+    walks = int(ln.numel())
+    hops = (tokens - walks) // 2
+    early = int((lens < width).sum().item())
+    gathered = 16 * hops + 8 * early + 4 * num_start
+    written = walks * (4 * width + 4)
+    return gathered + written, hops, tokens
+
+
+def traffic_from_profile(num_walks: int):
+    """HBM bytes per walk launch from the committed rocprofv3 --pmc summary, scaled by
+    the copy-kernel calibration recorded there; None when absent or taken from other
+    kernel sources or another launch size."""
+    try:
+        with open(PMC_FILE) as fh:
+            pmc = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if pmc.get("kernel_source_hash") != kernel_source_hash() or pmc.get("num_walks") != num_walks:
+        return None
+    return pmc.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, s, p, o, target_seconds: float):
+    """The CPU oracle, untuned, single-threaded, on a bounded sample of the workload."""
+    import numpy as np
+    import oracle
+    V, P = w.num_entities, w.num_predicates
+    t0 = time.perf_counter()
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    t_build = time.perf_counter() - t0
+    starts = oracle.nonsink_starts(rp, V)
+    num_walks = len(starts) * w.walks_per_node
+    # size the sample from a short probe so the whole leg takes about target_seconds
+    probe = min(num_walks, 20_000)
+    t0 = time.perf_counter()
+    oracle.random_walks(rp, ed, V, P, starts, w.walks_per_node, w.depth, 42, 0, probe)
+    rate = probe / max(time.perf_counter() - t0, 1e-9)
+    sample = int(min(num_walks, max(probe, rate * target_seconds)))
+    t0 = time.perf_counter()
+    _, ln = oracle.random_walks(rp, ed, V, P, starts, w.walks_per_node, w.depth, 42, 0, sample)
+    t_walk = time.perf_counter() - t0
+    tokens = int(ln.astype(np.int64).sum())
+    # the CSR build is charged in proportion to the sampled share of the walks
+    t_step_share = t_walk + t_build * sample / num_walks
+    return {
+        "value": tokens / t_step_share,
+        "unit": "tokens/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"oracle CSR build over all {w.num_triples:,} triples ({t_build:.2f} s, charged "
+                   f"pro rata) + the first {sample:,} of {num_walks:,} walks ({t_walk:.2f} s), "
+                   f"single thread on {os.cpu_count()} visible host cores"),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="powerlaw_20m")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="launch one plain device copy of this size first (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the walks would shard by walk-id range over replicated CSRs with no exchange)",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2508_01073_amd as rd
+    import synth
+
+    if not torch.cuda.is_available():
+        print("bench.py: no HIP device visible", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda:0")
+    w = synth.WORKLOADS[args.workload]
+    V, P, d, wpn = w.num_entities, w.num_predicates, w.depth, w.walks_per_node
+    s, p, o = synth.triples(w)
+    T = int(s.shape[0])
+    subj = torch.from_numpy(s).to(dev)
+    pred = torch.from_numpy(p).to(dev)
+    obj = torch.from_numpy(o).to(dev)
+
+    # Everything the step writes is allocated once, outside the timed region.
+    row_ptr = torch.empty(V + 1, dtype=torch.int32, device=dev)
+    edges = torch.empty((T, 2), dtype=torch.int32, device=dev)
+    ws_build = torch.empty(max(rd.rdf2v_build_csr_workspace_size(T, V), 1), dtype=torch.uint8, device=dev)
+    ws_starts = torch.empty(rd.rdf2v_nonsink_starts_workspace_size(V), dtype=torch.uint8, device=dev)
+    starts = torch.empty(V, dtype=torch.int32, device=dev)
+    count = torch.empty(1, dtype=torch.int64, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    max_walks = V * wpn
+    width = 2 * d + 1
+    tokens = torch.empty((max_walks, width), dtype=torch.int32, device=dev)
+    lens = torch.empty(max_walks, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    if args.copy_probe_mib > 0:
+        a = torch.ones(args.copy_probe_mib << 18, dtype=torch.int32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def step(record):
+        e0, e1, e2, e3 = ev(), ev(), ev(), ev()
+        e0.record(stream)
+        csr = rd.rdf2v_build_csr(subj, pred, obj, V, P, workspace=ws_build, status=status,
+                                 row_ptr=row_ptr, edges=edges, stream=stream)
+        e1.record(stream)
+        st, cnt = rd.rdf2v_nonsink_starts(csr, workspace=ws_starts, starts=starts, count=count,
+                                          stream=stream, sync=False)
+        n_start = int(cnt.item())
+        e2.record(stream)
+        n_walks = n_start * wpn
+        rd.rdf2v_random_walks(csr, st[:n_start], wpn, d, 42, 0, n_walks, tokens=tokens[:n_walks],
+                              lens=lens[:n_walks], status=status, stream=stream)
+        e3.record(stream)
+        record.append((e0, e1, e2, e3, n_start))
+
+    warm = []
+    for _ in range(max(args.warmup, 1)):
+        step(warm)
+    torch.cuda.synchronize()
+    rd.check_device_status(status, "warmup")
+    n_start = warm[-1][4]
+    n_walks = n_start * wpn
+    ub, hops, ntok = useful_bytes(lens[:n_walks], d, n_start)
+
+    rec = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(rec)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    rd.check_device_status(status, "timed steps")
+
+    elapsed = t1 - t0
+    ms_step = 1e3 * elapsed / args.steps
+    build_ms = float(np.mean([a.elapsed_time(b) for a, b, _, _, _ in rec]))
+    starts_ms = float(np.mean([b.elapsed_time(c) for _, b, c, _, _ in rec]))
+    walk_ms = float(np.mean([c.elapsed_time(e) for _, _, c, e, _ in rec]))
+    achieved = ub / (walk_ms * 1e-3) / 1e9
+    traffic = traffic_from_profile(n_walks)
+
+    out = {
+        "metric": METRIC,
+        "value": ntok * args.steps / elapsed,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "num_entities": V, "num_predicates": P, "num_triples": T,
+            "graph": w.kind, "depth": d, "walks_per_node": wpn, "num_start": n_start,
+            "num_walks": n_walks, "seed": 42,
+        },
+        "roofline": {
+            "kernel": "random_walk_kernel",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "useful_bytes_per_launch": ub,
+        },
+        "walk_kernel_ms": walk_ms,
+        "build_csr_ms": build_ms,
+        "nonsink_starts_ms": starts_ms,
+        "valid_tokens_per_step": ntok,
+        "hops_per_step": hops,
+        "walk_kernel_tokens_per_s": ntok / (walk_ms * 1e-3),
+        "walk_kernel_hops_per_s": hops / (walk_ms * 1e-3),
+        "padded_token_slots_per_s": n_walks * width / (walk_ms * 1e-3),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, s, p, o, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

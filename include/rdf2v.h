@@ -1,0 +1,165 @@
+/*
+ * rdf2v.h - C ABI of the MI355X (gfx950) RDF2vec random-walk corpus library.
+ *
+ * RDF2vec first extracts a corpus of graph walks from a knowledge graph and
+ * then trains Word2Vec on it (gpuRDF2vec, Boeckling & Paulheim, arXiv
+ * 2508.01073, Sec. 2). This library is the walk-extraction step for random
+ * walks: it builds a subject-indexed graph from id triples and runs
+ * walks_per_node uniform random walks of at most `depth` hops from each start
+ * entity, emitting each walk as an entity/predicate token row padded with -1
+ * (Sec. 3.1), with walks launched all at once rather than entity by entity
+ * (Sec. 4.1).
+ *
+ * Conventions shared by every call:
+ *  - Ids are int32. Entities are 0..num_entities-1, predicates are
+ *    0..num_predicates-1; in walk rows an entity's token is its id and a
+ *    predicate's token is num_entities + its id (Sec. 3.1: every entity and
+ *    predicate is tokenised to an integer id). num_entities + num_predicates
+ *    must stay below 2^31.
+ *  - All array arguments are DEVICE pointers to caller-owned memory unless
+ *    stated otherwise. The library never allocates, frees or keeps device
+ *    memory and keeps no global state; calls on different streams may overlap.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream). Every
+ *    call only enqueues work on it and returns without synchronising.
+ *  - Errors that the host can see (null pointers, negative or oversized
+ *    counts, workspace too small) are returned synchronously and nothing is
+ *    enqueued. Errors that only the device can see (ids out of range, an
+ *    inconsistent CSR) are ORed as RDF2V_STATUS_* bits into *status_dev, a
+ *    device int32 that the caller zeroes beforehand and reads after the stream
+ *    has synchronised; status_dev may be NULL, in which case such errors are
+ *    not reported. After a device-side error the outputs are unspecified, but
+ *    every memory access stays inside the buffers described here.
+ */
+#ifndef RDF2V_H_
+#define RDF2V_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rdf2v_status {
+  RDF2V_OK = 0,
+  RDF2V_ERR_INVALID_ARGUMENT = 1, /* null pointer, negative count, depth outside [0, RDF2V_MAX_DEPTH], walk range outside the corpus */
+  RDF2V_ERR_ID_OUT_OF_RANGE = 2,  /* an id the host can already see is out of range (e.g. triples with num_entities == 0) */
+  RDF2V_ERR_TOO_LARGE = 3,        /* num_triples >= 2^31, num_entities + num_predicates >= 2^31, walk counts overflowing int64 */
+  RDF2V_ERR_WORKSPACE = 4,        /* workspace NULL or smaller than the matching *_workspace_size() */
+  RDF2V_ERR_HIP = 5               /* a HIP launch or runtime call failed */
+} rdf2v_status;
+
+/* Bits ORed into *status_dev by the kernels. */
+#define RDF2V_STATUS_ID_OUT_OF_RANGE 0x1 /* a subject/object/start id >= num_entities or < 0, or a predicate id out of range */
+#define RDF2V_STATUS_BAD_CSR 0x2         /* row_ptr not non-decreasing within [0, num_edges] */
+
+/* Longest walk, in hops. A walk row holds 2 * depth + 1 tokens. */
+#define RDF2V_MAX_DEPTH 64
+
+/*
+ * A read-only VIEW of a subject-indexed CSR in device memory, as written by
+ * rdf2v_build_csr:
+ *   row_ptr[num_entities + 1]: int32, row_ptr[0] = 0, non-decreasing,
+ *                              row_ptr[num_entities] = num_edges.
+ *   edges[num_edges][2]:       int32 (predicate, object) out-edge records of
+ *                              entity v at rows row_ptr[v] .. row_ptr[v+1]-1;
+ *                              8-byte aligned.
+ * Duplicate triples and self-loops are separate records.
+ */
+typedef struct rdf2v_csr {
+  int32_t num_entities;
+  int32_t num_predicates;
+  int64_t num_edges;
+  const int32_t *row_ptr;
+  const int32_t *edges;
+} rdf2v_csr;
+
+/*
+ * Bytes of device workspace rdf2v_build_csr needs for these sizes (0 when
+ * num_triples == 0). Pure host function.
+ */
+size_t rdf2v_build_csr_workspace_size(int64_t num_triples, int32_t num_entities);
+
+/*
+ * Triples -> subject-indexed CSR (the graph the walks traverse; gpuRDF2vec
+ * Sec. 3.1 loads the tokenised triples into device memory as a graph).
+ *
+ *   subj, pred, obj   [num_triples] int32 ids (device).
+ *   row_ptr_out       [num_entities + 1] int32 (device), written.
+ *   edges_out         [num_triples][2] int32 (predicate, object) (device),
+ *                     written; 8-byte aligned; must not alias the inputs.
+ *   workspace         device scratch of at least
+ *                     rdf2v_build_csr_workspace_size(num_triples, num_entities)
+ *                     bytes, 256-byte aligned; contents clobbered.
+ *   status_dev        device int32 or NULL (RDF2V_STATUS_ID_OUT_OF_RANGE).
+ *
+ * Inside every row the records keep the input order of their triples (a
+ * stable sort by subject), so the result is deterministic and equal to a
+ * sequential counting sort. Runs as histogram, scan and stable-scatter passes
+ * of an LSD radix sort on the subject id followed by a row-offset kernel.
+ */
+rdf2v_status rdf2v_build_csr(const int32_t *subj, const int32_t *pred, const int32_t *obj,
+                             int64_t num_triples, int32_t num_entities, int32_t num_predicates,
+                             int32_t *row_ptr_out, int32_t *edges_out, void *workspace,
+                             size_t workspace_bytes, int32_t *status_dev, void *stream);
+
+/* Bytes of device workspace rdf2v_nonsink_starts needs. Pure host function. */
+size_t rdf2v_nonsink_starts_workspace_size(int32_t num_entities);
+
+/*
+ * The default start set: every entity with at least one out-edge, ascending
+ * (the paper starts walks from all entities when no start list is given,
+ * Sec. 3.3; an entity without out-edges would only give a one-token walk).
+ *
+ *   starts_out  [num_entities] int32 (device): the first *count_out entries
+ *               are written.
+ *   count_out   one int64 in device memory: the number of start entities.
+ *   workspace   device scratch, rdf2v_nonsink_starts_workspace_size() bytes.
+ */
+rdf2v_status rdf2v_nonsink_starts(const rdf2v_csr *csr, int32_t *starts_out, int64_t *count_out,
+                                  void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Uniform random walks (gpuRDF2vec Sec. 2: iterative random choice of the
+ * next hop; Sec. 3.1: triple-based token rows padded with -1; Sec. 4.1: all
+ * walks of all start entities launched together).
+ *
+ * The corpus has num_walks = num_start * walks_per_node walks; walk w starts
+ * at start_nodes[w / walks_per_node]. This call computes walks
+ * w = walk_begin .. walk_begin + walk_count - 1 into rows r = w - walk_begin,
+ * so a corpus can be produced in batches and any batch recomputed on its own.
+ *
+ * Walk w, from entity e_0 = start_nodes[w / walks_per_node], for hops
+ * h = 0 .. depth-1: if e_h has no out-edge the walk ends; otherwise with
+ * u = word (h mod 4) of Philox4x32-10(key = seed, counter = (h / 4, w)) (the
+ * 64-bit seed as key words lo, hi; the counter words are lo, hi of h / 4 then
+ * lo, hi of w; Salmon et al., SC'11), the walk takes out-edge record
+ * k = floor(u * deg(e_h) / 2^32) of e_h's row, (p, x), and appends tokens
+ * num_entities + p and x; e_{h+1} = x.
+ *
+ *   csr           view of a CSR as rdf2v_build_csr writes it (host pointer to
+ *                 the struct; the arrays it points to are device memory).
+ *   start_nodes   [num_start] int32 entity ids (device); duplicates and sinks
+ *                 allowed.
+ *   depth         hops per walk, 0 .. RDF2V_MAX_DEPTH.
+ *   tokens_out    [walk_count][2 * depth + 1] int32 (device), row-major:
+ *                 e_0, V+p_0, e_1, V+p_1, ..., then -1 after the walk's end.
+ *   len_out       [walk_count] int32 (device): valid tokens, 2 * hops + 1.
+ *   status_dev    device int32 or NULL (RDF2V_STATUS_* bits).
+ *
+ * walks_per_node == 0 or walk_count == 0 enqueues nothing and returns
+ * RDF2V_OK.
+ */
+rdf2v_status rdf2v_random_walks(const rdf2v_csr *csr, const int32_t *start_nodes, int64_t num_start,
+                                int32_t walks_per_node, int32_t depth, uint64_t seed,
+                                int64_t walk_begin, int64_t walk_count, int32_t *tokens_out,
+                                int32_t *len_out, int32_t *status_dev, void *stream);
+
+/* Static, human-readable name of a status code. */
+const char *rdf2v_status_string(rdf2v_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RDF2V_H_ */

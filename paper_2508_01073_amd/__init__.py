@@ -1,0 +1,224 @@
+"""MI355X-native RDF2vec random-walk corpus extraction.
+
+Python binding of ``librdf2v.so`` (HIP kernels for gfx950 behind the C ABI in
+``include/rdf2v.h``). The functions carry the C names and only marshal
+arguments: PyTorch supplies device memory and the stream, every step of the
+computation runs in the library's kernels. There is no CPU fallback: every call
+raises if the library has not been built (``python -m paper_2508_01073_amd.build``),
+and calls fail if no GPU is present.
+
+Walk extraction follows gpuRDF2vec (Boeckling & Paulheim, arXiv 2508.01073):
+uniform random walks (Sec. 2) emitted as entity/predicate token rows padded
+with -1 (Sec. 3.1), all walks of all start entities launched together
+(Sec. 4.1), with walk depth, walks per entity and seed as in Sec. 3.3.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+__all__ = [
+    "Csr", "Rdf2vError", "RDF2V_MAX_DEPTH", "RDF2V_STATUS_ID_OUT_OF_RANGE", "RDF2V_STATUS_BAD_CSR",
+    "rdf2v_build_csr_workspace_size", "rdf2v_build_csr", "rdf2v_nonsink_starts_workspace_size",
+    "rdf2v_nonsink_starts", "rdf2v_random_walks", "rdf2v_status_string", "check_device_status",
+    "library_path",
+]
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librdf2v.so")
+
+RDF2V_OK = 0
+RDF2V_ERR_INVALID_ARGUMENT = 1
+RDF2V_ERR_ID_OUT_OF_RANGE = 2
+RDF2V_ERR_TOO_LARGE = 3
+RDF2V_ERR_WORKSPACE = 4
+RDF2V_ERR_HIP = 5
+RDF2V_STATUS_ID_OUT_OF_RANGE = 0x1
+RDF2V_STATUS_BAD_CSR = 0x2
+RDF2V_MAX_DEPTH = 64
+
+_lib = None
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+class _CsrStruct(ctypes.Structure):
+    _fields_ = [("num_entities", ctypes.c_int32), ("num_predicates", ctypes.c_int32),
+                ("num_edges", ctypes.c_int64), ("row_ptr", ctypes.c_void_p),
+                ("edges", ctypes.c_void_p)]
+
+
+def _native():
+    """The loaded librdf2v.so; raises if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"{_LIB_PATH} is not built; run `python -m paper_2508_01073_amd.build`")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, i32, i64, u64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_size_t
+    csr_p = ctypes.POINTER(_CsrStruct)
+    lib.rdf2v_build_csr_workspace_size.argtypes = [i64, i32]
+    lib.rdf2v_build_csr_workspace_size.restype = sz
+    lib.rdf2v_build_csr.argtypes = [vp, vp, vp, i64, i32, i32, vp, vp, vp, sz, vp, vp]
+    lib.rdf2v_build_csr.restype = ctypes.c_int
+    lib.rdf2v_nonsink_starts_workspace_size.argtypes = [i32]
+    lib.rdf2v_nonsink_starts_workspace_size.restype = sz
+    lib.rdf2v_nonsink_starts.argtypes = [csr_p, vp, vp, vp, sz, vp]
+    lib.rdf2v_nonsink_starts.restype = ctypes.c_int
+    lib.rdf2v_random_walks.argtypes = [csr_p, vp, i64, i32, i32, u64, i64, i64, vp, vp, vp, vp]
+    lib.rdf2v_random_walks.restype = ctypes.c_int
+    lib.rdf2v_status_string.argtypes = [ctypes.c_int]
+    lib.rdf2v_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+class Rdf2vError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {rdf2v_status_string(status)} ({status})")
+        self.status = status
+
+
+def rdf2v_status_string(status: int) -> str:
+    return _native().rdf2v_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != RDF2V_OK:
+        raise Rdf2vError(status, where)
+
+
+def _dev_i32(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != torch.int32:
+        raise TypeError(f"{name} must be int32, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None or t.numel() == 0 else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device, stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+@dataclass
+class Csr:
+    """Subject-indexed CSR in device memory (see ``rdf2v_csr`` in rdf2v.h).
+
+    row_ptr: int32 [num_entities + 1]; edges: int32 [num_edges, 2] = (predicate, object)."""
+    row_ptr: torch.Tensor
+    edges: torch.Tensor
+    num_entities: int
+    num_predicates: int
+
+    @property
+    def num_edges(self) -> int:
+        return int(self.edges.shape[0])
+
+    def _c(self) -> _CsrStruct:
+        return _CsrStruct(self.num_entities, self.num_predicates, self.num_edges,
+                          self.row_ptr.data_ptr(), self.edges.data_ptr() if self.edges.numel() else None)
+
+
+def rdf2v_build_csr_workspace_size(num_triples: int, num_entities: int) -> int:
+    return int(_native().rdf2v_build_csr_workspace_size(num_triples, num_entities))
+
+
+def rdf2v_build_csr(subj: torch.Tensor, pred: torch.Tensor, obj: torch.Tensor, num_entities: int,
+                    num_predicates: int, *, workspace: torch.Tensor | None = None,
+                    status: torch.Tensor | None = None, stream=None,
+                    row_ptr: torch.Tensor | None = None, edges: torch.Tensor | None = None) -> Csr:
+    """Triples (device int32 [T] each) -> Csr. Rows keep the input order of their triples."""
+    _dev_i32(subj, "subj"); _dev_i32(pred, "pred"); _dev_i32(obj, "obj")
+    t = subj.shape[0]
+    if pred.shape[0] != t or obj.shape[0] != t:
+        raise ValueError("subj, pred and obj differ in length")
+    dev = subj.device
+    if row_ptr is None:
+        row_ptr = torch.empty(num_entities + 1, dtype=torch.int32, device=dev)
+    if edges is None:
+        edges = torch.empty((t, 2), dtype=torch.int32, device=dev)
+    need = rdf2v_build_csr_workspace_size(t, num_entities)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _native().rdf2v_build_csr(_ptr(subj), _ptr(pred), _ptr(obj), t, num_entities, num_predicates,
+                              _ptr(row_ptr), _ptr(edges), _ptr(workspace), ws_bytes, _ptr(status),
+                              _stream(dev, stream))
+    _check(st, "rdf2v_build_csr")
+    return Csr(row_ptr, edges, num_entities, num_predicates)
+
+
+def rdf2v_nonsink_starts_workspace_size(num_entities: int) -> int:
+    return int(_native().rdf2v_nonsink_starts_workspace_size(num_entities))
+
+
+def rdf2v_nonsink_starts(csr: Csr, *, workspace: torch.Tensor | None = None, stream=None,
+                         starts: torch.Tensor | None = None, count: torch.Tensor | None = None,
+                         sync: bool = True):
+    """Entities with out-degree >= 1, ascending. With sync=True returns the int32 tensor of
+    start ids (one device-to-host read of the count); else (starts, count_device_int64)."""
+    dev = csr.row_ptr.device
+    if starts is None:
+        starts = torch.empty(max(csr.num_entities, 1), dtype=torch.int32, device=dev)
+    if count is None:
+        count = torch.empty(1, dtype=torch.int64, device=dev)
+    if workspace is None:
+        workspace = torch.empty(rdf2v_nonsink_starts_workspace_size(csr.num_entities),
+                                dtype=torch.uint8, device=dev)
+    c = csr._c()
+    st = _native().rdf2v_nonsink_starts(ctypes.byref(c), _ptr(starts), _ptr(count), _ptr(workspace),
+                                   workspace.numel(), _stream(dev, stream))
+    _check(st, "rdf2v_nonsink_starts")
+    if not sync:
+        return starts, count
+    return starts[: int(count.item())]
+
+
+def rdf2v_random_walks(csr: Csr, start_nodes: torch.Tensor, walks_per_node: int, depth: int,
+                       seed: int, walk_begin: int = 0, walk_count: int | None = None, *,
+                       tokens: torch.Tensor | None = None, lens: torch.Tensor | None = None,
+                       status: torch.Tensor | None = None, stream=None):
+    """Walks [walk_begin, walk_begin + walk_count) -> (tokens int32 [walk_count, 2*depth+1],
+    lens int32 [walk_count]). Walk w starts at start_nodes[w // walks_per_node]."""
+    _dev_i32(start_nodes, "start_nodes")
+    dev = start_nodes.device
+    num_walks = start_nodes.shape[0] * walks_per_node
+    if walk_count is None:
+        walk_count = num_walks - walk_begin
+    width = 2 * depth + 1
+    if tokens is None:
+        tokens = torch.empty((max(walk_count, 0), max(width, 1)), dtype=torch.int32, device=dev)
+    if lens is None:
+        lens = torch.empty(max(walk_count, 0), dtype=torch.int32, device=dev)
+    if walk_count > 0 and (tokens.numel() < walk_count * width or lens.numel() < walk_count):
+        raise ValueError("output buffers too small for walk_count rows")
+    c = csr._c()
+    st = _native().rdf2v_random_walks(ctypes.byref(c), _ptr(start_nodes), start_nodes.shape[0],
+                                 walks_per_node, depth, ctypes.c_uint64(seed & (2**64 - 1)),
+                                 walk_begin, walk_count, _ptr(tokens), _ptr(lens), _ptr(status),
+                                 _stream(dev, stream))
+    _check(st, "rdf2v_random_walks")
+    return tokens, lens
+
+
+def check_device_status(status: torch.Tensor, where: str = "device") -> None:
+    """Raise if a device status word (zeroed before the calls) has any bit set."""
+    v = int(status.item())
+    if v != 0:
+        bits = [n for b, n in [(RDF2V_STATUS_ID_OUT_OF_RANGE, "ID_OUT_OF_RANGE"),
+                               (RDF2V_STATUS_BAD_CSR, "BAD_CSR")] if v & b]
+        raise Rdf2vError(RDF2V_ERR_ID_OUT_OF_RANGE, f"{where}: status bits {'|'.join(bits) or v}")

@@ -1,0 +1,118 @@
+// extern "C" entry points: host-side argument checks, then the launchers.
+// The declarations, argument meanings and error behaviour are in rdf2v.h.
+
+#include <climits>
+
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace {
+
+constexpr int64_t kInt32Limit = int64_t(1) << 31;
+
+bool id_space_too_large(int32_t num_entities, int32_t num_predicates) {
+  return int64_t(num_entities) + int64_t(num_predicates) >= kInt32Limit;
+}
+
+}  // namespace
+
+RDF2V_API size_t rdf2v_build_csr_workspace_size(int64_t num_triples, int32_t num_entities) {
+  if (num_triples <= 0 || num_triples >= kInt32Limit || num_entities < 0) return 0;
+  return rdf2v::plan_csr_build(num_triples, num_entities).bytes;
+}
+
+RDF2V_API rdf2v_status rdf2v_build_csr(const int32_t *subj, const int32_t *pred, const int32_t *obj,
+                                       int64_t num_triples, int32_t num_entities,
+                                       int32_t num_predicates, int32_t *row_ptr_out,
+                                       int32_t *edges_out, void *workspace, size_t workspace_bytes,
+                                       int32_t *status_dev, void *stream) {
+  if (num_triples < 0 || num_entities < 0 || num_predicates < 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (row_ptr_out == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (num_triples >= kInt32Limit || id_space_too_large(num_entities, num_predicates))
+    return RDF2V_ERR_TOO_LARGE;
+  if (num_triples > 0) {
+    if (subj == nullptr || pred == nullptr || obj == nullptr || edges_out == nullptr)
+      return RDF2V_ERR_INVALID_ARGUMENT;
+    if ((reinterpret_cast<uintptr_t>(edges_out) & 7) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
+    // Every subject must be < num_entities; with no entities that is impossible.
+    if (num_entities == 0 || num_predicates == 0) return RDF2V_ERR_ID_OUT_OF_RANGE;
+  }
+  const rdf2v::SortPlan plan = rdf2v::plan_csr_build(num_triples, num_entities);
+  if (plan.bytes > 0) {
+    if (workspace == nullptr || workspace_bytes < plan.bytes) return RDF2V_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return RDF2V_ERR_WORKSPACE;
+  }
+  return rdf2v::launch_csr_build(subj, pred, obj, num_triples, num_entities, num_predicates,
+                                 row_ptr_out, edges_out, workspace, plan, status_dev,
+                                 static_cast<hipStream_t>(stream));
+}
+
+RDF2V_API size_t rdf2v_nonsink_starts_workspace_size(int32_t num_entities) {
+  return rdf2v::nonsink_workspace_bytes(num_entities);
+}
+
+RDF2V_API rdf2v_status rdf2v_nonsink_starts(const rdf2v_csr *csr, int32_t *starts_out,
+                                            int64_t *count_out, void *workspace,
+                                            size_t workspace_bytes, void *stream) {
+  if (csr == nullptr || count_out == nullptr || csr->row_ptr == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (csr->num_entities < 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (csr->num_entities > 0 && starts_out == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  const size_t need = rdf2v::nonsink_workspace_bytes(csr->num_entities);
+  if (workspace == nullptr || workspace_bytes < need) return RDF2V_ERR_WORKSPACE;
+  return rdf2v::launch_nonsink_starts(csr->row_ptr, csr->num_entities, starts_out, count_out,
+                                      workspace, static_cast<hipStream_t>(stream));
+}
+
+RDF2V_API rdf2v_status rdf2v_random_walks(const rdf2v_csr *csr, const int32_t *start_nodes,
+                                          int64_t num_start, int32_t walks_per_node, int32_t depth,
+                                          uint64_t seed, int64_t walk_begin, int64_t walk_count,
+                                          int32_t *tokens_out, int32_t *len_out,
+                                          int32_t *status_dev, void *stream) {
+  if (csr == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (csr->num_entities < 0 || csr->num_predicates < 0 || csr->num_edges < 0)
+    return RDF2V_ERR_INVALID_ARGUMENT;
+  if (num_start < 0 || walks_per_node < 0 || depth < 0 || depth > RDF2V_MAX_DEPTH)
+    return RDF2V_ERR_INVALID_ARGUMENT;
+  if (walk_begin < 0 || walk_count < 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (csr->num_edges >= kInt32Limit || id_space_too_large(csr->num_entities, csr->num_predicates))
+    return RDF2V_ERR_TOO_LARGE;
+  if (walks_per_node > 0 && num_start > INT64_MAX / walks_per_node) return RDF2V_ERR_TOO_LARGE;
+  const int64_t num_walks = num_start * int64_t(walks_per_node);
+  if (walk_begin > num_walks || walk_count > num_walks - walk_begin) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (walk_count == 0) return RDF2V_OK;
+  if (start_nodes == nullptr || tokens_out == nullptr || len_out == nullptr || csr->row_ptr == nullptr)
+    return RDF2V_ERR_INVALID_ARGUMENT;
+  if (csr->num_edges > 0 && csr->edges == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if ((reinterpret_cast<uintptr_t>(csr->edges) & 7) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (walk_count > INT64_MAX / (2 * int64_t(depth) + 1)) return RDF2V_ERR_TOO_LARGE;
+
+  rdf2v::WalkArgs a;
+  a.row_ptr = csr->row_ptr;
+  a.edges = csr->edges;
+  a.start = start_nodes;
+  a.tokens = tokens_out;
+  a.lens = len_out;
+  a.status = status_dev;
+  a.walk_begin = walk_begin;
+  a.walk_count = walk_count;
+  a.num_edges = csr->num_edges;
+  a.num_entities = csr->num_entities;
+  a.num_predicates = csr->num_predicates;
+  a.walks_per_node = walks_per_node;
+  a.depth = depth;
+  a.key_lo = uint32_t(seed);
+  a.key_hi = uint32_t(seed >> 32);
+  return rdf2v::launch_random_walks(a, static_cast<hipStream_t>(stream));
+}
+
+RDF2V_API const char *rdf2v_status_string(rdf2v_status status) {
+  switch (status) {
+    case RDF2V_OK: return "RDF2V_OK";
+    case RDF2V_ERR_INVALID_ARGUMENT: return "RDF2V_ERR_INVALID_ARGUMENT";
+    case RDF2V_ERR_ID_OUT_OF_RANGE: return "RDF2V_ERR_ID_OUT_OF_RANGE";
+    case RDF2V_ERR_TOO_LARGE: return "RDF2V_ERR_TOO_LARGE";
+    case RDF2V_ERR_WORKSPACE: return "RDF2V_ERR_WORKSPACE";
+    case RDF2V_ERR_HIP: return "RDF2V_ERR_HIP";
+  }
+  return "RDF2V_UNKNOWN_STATUS";
+}

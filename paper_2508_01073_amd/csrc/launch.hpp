@@ -1,0 +1,54 @@
+// Host-side launchers of the library's kernels. The extern "C" entry points in
+// api.hip validate arguments and call these; each launcher only enqueues.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "rdf2v.h"
+
+namespace rdf2v {
+
+// Layout of the rdf2v_build_csr workspace for (num_triples, num_entities).
+struct SortPlan {
+  int passes = 0;      // LSD radix passes over the subject id
+  int digit_bits = 0;  // bits per pass (<= 8)
+  int64_t tiles = 0;   // 4096-triple tiles
+  int64_t count_len = 0;     // digit-major count table length = bins * tiles
+  int64_t count_blocks = 0;  // scan blocks over the count table
+  size_t off_keys_a = 0, off_keys_b = 0, off_payload = 0, off_counts = 0, off_partials = 0;
+  size_t bytes = 0;
+};
+SortPlan plan_csr_build(int64_t num_triples, int32_t num_entities);
+
+rdf2v_status launch_csr_build(const int32_t *subj, const int32_t *pred, const int32_t *obj,
+                              int64_t num_triples, int32_t num_entities, int32_t num_predicates,
+                              int32_t *row_ptr_out, int32_t *edges_out, void *workspace,
+                              const SortPlan &plan, int32_t *status_dev, hipStream_t stream);
+
+size_t nonsink_workspace_bytes(int32_t num_entities);
+rdf2v_status launch_nonsink_starts(const int32_t *row_ptr, int32_t num_entities, int32_t *starts_out,
+                                   int64_t *count_out, void *workspace, hipStream_t stream);
+
+struct WalkArgs {
+  const int32_t *row_ptr;
+  const int32_t *edges;  // (predicate, object) pairs, 8-byte aligned
+  const int32_t *start;
+  int32_t *tokens;
+  int32_t *lens;
+  int32_t *status;
+  int64_t walk_begin;
+  int64_t walk_count;
+  int64_t num_edges;
+  int32_t num_entities;
+  int32_t num_predicates;
+  int32_t walks_per_node;
+  int32_t depth;
+  uint32_t key_lo;
+  uint32_t key_hi;
+};
+rdf2v_status launch_random_walks(const WalkArgs &args, hipStream_t stream);
+
+}  // namespace rdf2v

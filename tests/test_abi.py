@@ -1,0 +1,157 @@
+"""The C-ABI library loads, exports every function include/rdf2v.h declares, and
+rejects bad arguments on the host before touching a GPU (no compute calls here).
+
+Every call below fails host-side validation, which returns before any HIP API
+call, so the dummy device pointers are never dereferenced.
+"""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rdf2v.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rdf2v_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2508_01073_amd as pkg
+    return pkg._native(), pkg
+
+
+def test_header_declares_the_calls():
+    names = _declared_functions()
+    for n in ["rdf2v_build_csr", "rdf2v_build_csr_workspace_size", "rdf2v_random_walks",
+              "rdf2v_nonsink_starts", "rdf2v_nonsink_starts_workspace_size", "rdf2v_status_string"]:
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    so, pkg = lib
+    out = subprocess.run(["nm", "-D", "--defined-only", pkg.library_path()], stdout=subprocess.PIPE,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (rdf2v_\w+)", out))
+    for name in _declared_functions():
+        assert name in exported, name
+        assert getattr(so, name) is not None
+    # nothing beyond the declared C ABI is exported
+    assert exported == set(_declared_functions())
+
+
+def test_header_compiles_as_c():
+    res = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-x", "c", HEADER],
+                         stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    assert res.returncode == 0, res.stdout
+
+
+def test_status_strings(lib):
+    _, pkg = lib
+    assert pkg.rdf2v_status_string(0) == "RDF2V_OK"
+    assert pkg.rdf2v_status_string(4) == "RDF2V_ERR_WORKSPACE"
+    assert pkg.rdf2v_status_string(99) == "RDF2V_UNKNOWN_STATUS"
+
+
+def test_workspace_sizes(lib):
+    _, pkg = lib
+    assert pkg.rdf2v_build_csr_workspace_size(0, 10) == 0
+    a = pkg.rdf2v_build_csr_workspace_size(5000, 1000)
+    b = pkg.rdf2v_build_csr_workspace_size(20_000_000, 1_000_000)
+    assert 0 < a < b and a % 256 == 0 and b % 256 == 0
+    # keys x2 + payload = 16 B per triple, plus the radix count table
+    assert b >= 16 * 20_000_000
+    assert pkg.rdf2v_build_csr_workspace_size(2**31, 10) == 0
+    assert pkg.rdf2v_nonsink_starts_workspace_size(0) >= 4
+
+
+FAKE = ctypes.c_void_p(1 << 40)        # never dereferenced: validation fails first
+FAKE8 = ctypes.c_void_p(1 << 40)
+
+
+def _csr(pkg, V=10, P=3, E=20, row_ptr=FAKE, edges=FAKE8):
+    return pkg._CsrStruct(V, P, E, row_ptr, edges)
+
+
+def _walk(lib, csr, start=FAKE, S=5, wpn=2, depth=4, wb=0, wc=None, tokens=FAKE, lens=FAKE):
+    so, pkg = lib
+    wc = S * wpn - wb if wc is None else wc
+    return so.rdf2v_random_walks(ctypes.byref(csr) if csr is not None else None, start, S, wpn, depth,
+                                 42, wb, wc, tokens, lens, None, None)
+
+
+def test_walk_argument_validation(lib):
+    so, pkg = lib
+    c = _csr(pkg)
+    E_INV, E_BIG = pkg.RDF2V_ERR_INVALID_ARGUMENT, pkg.RDF2V_ERR_TOO_LARGE
+    assert _walk(lib, None) == E_INV
+    assert _walk(lib, c, depth=65) == E_INV
+    assert _walk(lib, c, depth=-1) == E_INV
+    assert _walk(lib, c, S=-1) == E_INV
+    assert _walk(lib, c, wpn=-2) == E_INV
+    assert _walk(lib, c, wb=-1) == E_INV
+    assert _walk(lib, c, wb=3, wc=8) == E_INV           # past the end of the corpus
+    assert _walk(lib, c, wb=11, wc=0) == E_INV          # begins past the end
+    assert _walk(lib, c, start=None) == E_INV
+    assert _walk(lib, c, tokens=None) == E_INV
+    assert _walk(lib, c, lens=None) == E_INV
+    assert _walk(lib, _csr(pkg, row_ptr=None)) == E_INV
+    assert _walk(lib, _csr(pkg, edges=ctypes.c_void_p((1 << 40) + 4))) == E_INV   # not 8-byte aligned
+    assert _walk(lib, _csr(pkg, V=-1)) == E_INV
+    assert _walk(lib, _csr(pkg, E=2**31)) == E_BIG
+    assert _walk(lib, _csr(pkg, V=2**30, P=2**30)) == E_BIG
+    assert _walk(lib, c, S=2**62, wpn=4, wc=1) == E_BIG
+    # nothing to do is not an error and launches nothing
+    assert _walk(lib, c, wpn=0) == pkg.RDF2V_OK
+    assert _walk(lib, c, wc=0) == pkg.RDF2V_OK
+    assert _walk(lib, c, S=0) == pkg.RDF2V_OK
+
+
+def test_build_argument_validation(lib):
+    so, pkg = lib
+    f = so.rdf2v_build_csr
+    ws = pkg.rdf2v_build_csr_workspace_size(100, 10)
+    WS = ctypes.c_void_p(1 << 41)
+    assert f(FAKE, FAKE, FAKE, -1, 10, 3, FAKE, FAKE8, WS, ws, None, None) == pkg.RDF2V_ERR_INVALID_ARGUMENT
+    assert f(FAKE, FAKE, FAKE, 100, -1, 3, FAKE, FAKE8, WS, ws, None, None) == pkg.RDF2V_ERR_INVALID_ARGUMENT
+    assert f(FAKE, FAKE, FAKE, 100, 10, 3, None, FAKE8, WS, ws, None, None) == pkg.RDF2V_ERR_INVALID_ARGUMENT
+    assert f(None, FAKE, FAKE, 100, 10, 3, FAKE, FAKE8, WS, ws, None, None) == pkg.RDF2V_ERR_INVALID_ARGUMENT
+    assert f(FAKE, FAKE, FAKE, 100, 10, 3, FAKE, ctypes.c_void_p((1 << 40) + 4), WS, ws, None, None) \
+        == pkg.RDF2V_ERR_INVALID_ARGUMENT
+    assert f(FAKE, FAKE, FAKE, 2**31, 10, 3, FAKE, FAKE8, WS, ws, None, None) == pkg.RDF2V_ERR_TOO_LARGE
+    assert f(FAKE, FAKE, FAKE, 100, 2**31 - 2, 3, FAKE, FAKE8, WS, ws, None, None) == pkg.RDF2V_ERR_TOO_LARGE
+    assert f(FAKE, FAKE, FAKE, 100, 0, 3, FAKE, FAKE8, WS, ws, None, None) == pkg.RDF2V_ERR_ID_OUT_OF_RANGE
+    assert f(FAKE, FAKE, FAKE, 100, 10, 3, FAKE, FAKE8, None, ws, None, None) == pkg.RDF2V_ERR_WORKSPACE
+    assert f(FAKE, FAKE, FAKE, 100, 10, 3, FAKE, FAKE8, WS, ws - 1, None, None) == pkg.RDF2V_ERR_WORKSPACE
+    assert f(FAKE, FAKE, FAKE, 100, 10, 3, FAKE, FAKE8, ctypes.c_void_p((1 << 41) + 64), ws, None, None) \
+        == pkg.RDF2V_ERR_WORKSPACE
+
+
+def test_nonsink_argument_validation(lib):
+    so, pkg = lib
+    c = _csr(pkg)
+    need = pkg.rdf2v_nonsink_starts_workspace_size(10)
+    f = so.rdf2v_nonsink_starts
+    assert f(None, FAKE, FAKE, FAKE, need, None) == pkg.RDF2V_ERR_INVALID_ARGUMENT
+    assert f(ctypes.byref(c), FAKE, None, FAKE, need, None) == pkg.RDF2V_ERR_INVALID_ARGUMENT
+    assert f(ctypes.byref(c), None, FAKE, FAKE, need, None) == pkg.RDF2V_ERR_INVALID_ARGUMENT
+    assert f(ctypes.byref(c), FAKE, FAKE, None, need, None) == pkg.RDF2V_ERR_WORKSPACE
+    assert f(ctypes.byref(c), FAKE, FAKE, FAKE, need - 1, None) == pkg.RDF2V_ERR_WORKSPACE
+
+
+def test_binding_has_no_cpu_fallback(lib):
+    # The product package never imports the oracle and has no CPU path.
+    src_dir = os.path.join(ROOT, "paper_2508_01073_amd")
+    for dirpath, _, files in os.walk(src_dir):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".hpp", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, fn)).read()
+                assert "import oracle" not in text and "from oracle" not in text, fn
+                assert "rdf2v_oracle" not in text and "rdf2v_ref_" not in text, fn

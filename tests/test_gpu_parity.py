@@ -1,0 +1,259 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle, bit-exact.
+
+Small cases compare every output element; full-size workloads compare the
+whole CSR and start set, and walk rows on sampled windows (first, last/ragged,
+random, hub starts), plus properties that hold at any size on the device.
+"""
+
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2508_01073_amd as rd
+import synth
+from gpu_helpers import (assert_csr_equal, assert_rows_equal, check_walk_properties, compare_windows,
+                         device, gpu_csr, gpu_walks, new_status, say, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+# ----------------------------------------------------------------------------
+# Hand-built graphs, every element
+# ----------------------------------------------------------------------------
+
+def _hand_graphs():
+    g = {}
+    n = 7
+    g["chain"] = ([(i, i % 3, i + 1) for i in range(n - 1)], n, 3, [0, 3, 6])
+    g["star10"] = ([(0, j % 4, j + 1) for j in range(10)], 11, 4, [0, 5])
+    g["complete6"] = ([(v, (v + j) % 2, j) for v in range(6) for j in range(6)], 6, 2, list(range(6)))
+    rng = np.random.default_rng(11)
+    tr = [(int(a), int(b), int(c)) for a, b, c in zip(rng.integers(0, 8, 16), rng.integers(0, 3, 16),
+                                                       rng.integers(0, 8, 16))]
+    tr += [(0, 1, 0), (0, 1, 0), (3, 2, 3)]  # duplicates and self-loops
+    g["multi_selfloop"] = (tr, 9, 3, [0, 3, 8, 8, 1])  # entity 8 has no out-edge
+    g["sink_starts"] = ([(0, 0, 1)], 4, 1, [1, 2, 3, 0])
+    return g
+
+
+HAND = _hand_graphs()
+
+
+@pytest.mark.parametrize("name", sorted(HAND))
+@pytest.mark.parametrize("depth", [0, 1, 4, 5, 9, 17, 64])
+def test_hand_graph_parity(name, depth):
+    tr, V, P, starts = HAND[name]
+    say(f"[hand] {name} depth={depth}")
+    t = np.array(tr, dtype=np.int32)
+    rp, ed = oracle.build_csr(t[:, 0], t[:, 1], t[:, 2], V, P)
+    csr = gpu_csr(t[:, 0], t[:, 1], t[:, 2], V, P)
+    assert_csr_equal(csr, rp, ed)
+    wpn = 37
+    for seed in (42, 2**63 + 5):
+        tok, ln = gpu_walks(csr, to_dev(starts), wpn, depth, seed)
+        tr_, lr_ = oracle.random_walks(rp, ed, V, P, np.array(starts), wpn, depth, seed)
+        assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, f"{name} seed {seed}")
+
+
+# ----------------------------------------------------------------------------
+# Random graphs spanning several 4096-triple tiles with ragged tails and 1..4
+# radix passes (entity id widths 1 .. 26 bits)
+# ----------------------------------------------------------------------------
+
+RANDOM_CASES = [
+    (1, 1, 5000), (2, 3, 1), (37, 1, 4096 * 3 + 17), (300, 7, 50_000), (256, 5, 8192),
+    (70_000, 11, 100_001), (2**25 + 3, 5, 20_000), (1_000, 20, 4095),
+]
+
+
+@pytest.mark.parametrize("V,P,T", RANDOM_CASES)
+def test_random_graph_parity(V, P, T):
+    say(f"[random] V={V} P={P} T={T}")
+    rng = np.random.default_rng(V * 31 + T)
+    s = rng.integers(0, V, T).astype(np.int32)
+    p = rng.integers(0, P, T).astype(np.int32)
+    o = rng.integers(0, V, T).astype(np.int32)
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    assert_csr_equal(csr, rp, ed)
+    starts = oracle.nonsink_starts(rp, V)
+    starts_gpu = rd.rdf2v_nonsink_starts(csr)
+    assert np.array_equal(starts_gpu.cpu().numpy(), starts)
+    for depth, wpn in [(4, 3), (8, 2), (16, 1), (33, 1)]:
+        sub = starts[:20_000]
+        tok, ln = gpu_walks(csr, to_dev(sub), wpn, depth, 42)
+        tr_, lr_ = oracle.random_walks(rp, ed, V, P, sub, wpn, depth, 42)
+        assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, f"depth {depth}")
+
+
+def test_powerlaw_small_with_sinks():
+    say("[powerlaw small] V=20000 T=300000 sinks 10%")
+    V, P = 20_000, 40
+    s, p, o = synth.powerlaw_triples(V, P, 300_000, sink_fraction=0.1)
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    assert_csr_equal(csr, rp, ed)
+    starts = oracle.nonsink_starts(rp, V)
+    tok, ln = gpu_walks(csr, to_dev(starts), 3, 16, 7)
+    tr_, lr_ = oracle.random_walks(rp, ed, V, P, starts, 3, 16, 7)
+    assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, "powerlaw small")
+
+
+# ----------------------------------------------------------------------------
+# The generated workloads
+# ----------------------------------------------------------------------------
+
+def test_tiny_uniform_full_parity():
+    w = synth.WORKLOADS["tiny_uniform"]
+    say(f"[workload] {w.describe()}")
+    s, p, o = synth.triples(w)
+    V, P = w.num_entities, w.num_predicates
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    assert_csr_equal(csr, rp, ed)
+    starts = oracle.nonsink_starts(rp, V)
+    starts_dev = rd.rdf2v_nonsink_starts(csr)
+    assert np.array_equal(starts_dev.cpu().numpy(), starts)
+    tok, ln = gpu_walks(csr, starts_dev, w.walks_per_node, w.depth, synth.WALK_SEED)
+    tr_, lr_ = oracle.random_walks(rp, ed, V, P, starts, w.walks_per_node, w.depth, synth.WALK_SEED)
+    assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, "tiny_uniform")
+
+
+def _windows(num_walks, wpn, starts, deg, rng, k=24, size=1024):
+    win = [(0, min(4096, num_walks)), (max(0, num_walks - 4093), min(4093, num_walks))]
+    for b in rng.integers(0, max(1, num_walks - size), k):
+        win.append((int(b), min(size, num_walks - int(b))))
+    # walks from the highest-degree start entities
+    for i in np.argsort(-deg[starts])[:4]:
+        win.append((int(i) * wpn, wpn))
+    return win
+
+
+@pytest.mark.parametrize("name", ["uniform_1m", "powerlaw_20m", "dense_10m"])
+def test_full_size_workload(name):
+    w = synth.WORKLOADS[name]
+    say(f"[workload] {w.describe()}")
+    s, p, o = synth.triples(w)
+    V, P = w.num_entities, w.num_predicates
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    assert_csr_equal(csr, rp, ed)
+    starts = oracle.nonsink_starts(rp, V)
+    starts_dev = rd.rdf2v_nonsink_starts(csr)
+    assert np.array_equal(starts_dev.cpu().numpy(), starts)
+    num_walks = len(starts) * w.walks_per_node
+    say(f"[workload] {name}: one launch of {num_walks} walks, depth {w.depth}")
+    tok, ln = gpu_walks(csr, starts_dev, w.walks_per_node, w.depth, synth.WALK_SEED)
+    check_walk_properties(tok, ln, starts_dev, w.walks_per_node, V, P, w.depth)
+    rng = np.random.default_rng(5)
+    n = compare_windows(csr, rp, ed, V, P, starts, w.walks_per_node, w.depth, synth.WALK_SEED, tok, ln,
+                        _windows(num_walks, w.walks_per_node, starts, np.diff(rp), rng))
+    say(f"[workload] {name}: {n} sampled rows bit-exact")
+
+
+# ----------------------------------------------------------------------------
+# Batching, determinism, status reporting, edge cases
+# ----------------------------------------------------------------------------
+
+def test_batches_concatenate_to_one_shot():
+    say("[batches] uniform 50k entities")
+    V, P = 50_000, 9
+    s, p, o = synth.uniform_triples(V, P, 400_000)
+    csr = gpu_csr(s, p, o, V, P)
+    starts_dev = rd.rdf2v_nonsink_starts(csr)
+    wpn, depth = 7, 6
+    total = starts_dev.shape[0] * wpn
+    full_t, full_l = gpu_walks(csr, starts_dev, wpn, depth, 42)
+    parts_t, parts_l, b = [], [], 0
+    for size in itertools.cycle([1, 255, 256, 257, 4099, 65_536, 100_003]):
+        if b >= total:
+            break
+        c = min(size, total - b)
+        t_, l_ = gpu_walks(csr, starts_dev, wpn, depth, 42, b, c)
+        parts_t.append(t_); parts_l.append(l_); b += c
+    assert torch.equal(torch.cat(parts_t), full_t) and torch.equal(torch.cat(parts_l), full_l)
+
+
+def test_repeat_runs_identical():
+    say("[repeat] powerlaw 200k entities")
+    V, P = 200_000, 30
+    s, p, o = synth.powerlaw_triples(V, P, 3_000_000)
+    c1 = gpu_csr(s, p, o, V, P)
+    c2 = gpu_csr(s, p, o, V, P)
+    assert torch.equal(c1.row_ptr, c2.row_ptr) and torch.equal(c1.edges, c2.edges)
+    st = rd.rdf2v_nonsink_starts(c1)
+    a = gpu_walks(c1, st, 5, 8, 42)
+    b = gpu_walks(c2, st, 5, 8, 42)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+def test_status_bits_for_bad_ids():
+    say("[status] out-of-range ids")
+    V, P = 10, 3
+    s = np.array([0, 1, 2, 3], np.int32); p = np.array([0, 1, 2, 0], np.int32)
+    o = np.array([1, 2, 3, 4], np.int32)
+    for bad in [("s", 10), ("o", 11), ("p", 3), ("s", -1)]:
+        ss, pp, oo = s.copy(), p.copy(), o.copy()
+        {"s": ss, "p": pp, "o": oo}[bad[0]][2] = bad[1]
+        st = new_status()
+        gpu_csr(ss, pp, oo, V, P, status=st)
+        assert int(st.item()) & rd.RDF2V_STATUS_ID_OUT_OF_RANGE, bad
+    csr = gpu_csr(s, p, o, V, P)
+    st = new_status()
+    rd.rdf2v_random_walks(csr, to_dev([0, 12]), 2, 3, 42, status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) & rd.RDF2V_STATUS_ID_OUT_OF_RANGE
+
+
+def test_inconsistent_csr_is_flagged_not_read():
+    say("[status] inconsistent CSR")
+    dev = device()
+    # row_ptr decreasing at entity 1 and past num_edges at entity 2: every gather is
+    # bounds-checked before it is issued, so the kernel only raises the status bit.
+    row_ptr = torch.tensor([0, 3, 1, 50, 4], dtype=torch.int32, device=dev)
+    edges = torch.tensor([[0, 1], [0, 2], [0, 1], [0, 3]], dtype=torch.int32, device=dev)
+    csr = rd.Csr(row_ptr, edges, 4, 1)
+    for start in (1, 2):
+        st = new_status()
+        tok, ln = rd.rdf2v_random_walks(csr, to_dev([start]), 1, 4, 42, status=st)
+        torch.cuda.synchronize()
+        assert int(st.item()) & rd.RDF2V_STATUS_BAD_CSR
+
+
+def test_empty_and_degenerate_inputs():
+    say("[edge] empty / degenerate")
+    dev = device()
+    e = torch.empty(0, dtype=torch.int32, device=dev)
+    csr = rd.rdf2v_build_csr(e, e, e, 5, 2)
+    torch.cuda.synchronize()
+    assert torch.equal(csr.row_ptr.cpu(), torch.zeros(6, dtype=torch.int32))
+    assert rd.rdf2v_nonsink_starts(csr).numel() == 0
+    tok, ln = gpu_walks(csr, to_dev([0, 4]), 3, 5, 42)
+    assert bool((ln == 1).all()) and torch.equal(tok[:, 0].cpu(), torch.tensor([0, 0, 0, 4, 4, 4], dtype=torch.int32))
+    assert bool((tok[:, 1:] == -1).all())
+    tok, ln = gpu_walks(csr, to_dev([0]), 0, 5, 42)
+    assert tok.shape[0] == 0 and ln.shape[0] == 0
+    csr0 = rd.rdf2v_build_csr(e, e, e, 0, 0)
+    torch.cuda.synchronize()
+    assert csr0.row_ptr.cpu().tolist() == [0]
+
+
+def test_unaligned_output_rows():
+    say("[edge] output pointer not 16-byte aligned")
+    V, P = 3000, 4
+    s, p, o = synth.uniform_triples(V, P, 20_000)
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    starts = oracle.nonsink_starts(rp, V)[:500]
+    depth, wpn = 5, 3
+    n = len(starts) * wpn
+    buf = torch.full((n * (2 * depth + 1) + 1,), 7, dtype=torch.int32, device=device())
+    tok = buf[1:].view(n, 2 * depth + 1)
+    lens = torch.empty(n, dtype=torch.int32, device=device())
+    gpu_walks(csr, to_dev(starts), wpn, depth, 42, tokens=tok, lens=lens)
+    tr_, lr_ = oracle.random_walks(rp, ed, V, P, starts, wpn, depth, 42)
+    assert_rows_equal(tok.cpu().numpy(), lens.cpu().numpy(), tr_, lr_, "unaligned")
+    assert int(buf[0].item()) == 7
