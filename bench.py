@@ -2,8 +2,9 @@
 """Benchmark: RDF2vec random-walk corpus extraction on one MI355X.
 
 One step is one pass of the whole path over inputs already resident in HBM:
-rdf2v_build_csr (triples -> CSR), rdf2v_nonsink_starts (start set) and
-rdf2v_random_walks (every walk of every start entity, one launch). The default
+rdf2v_build_csr (triples -> CSR), rdf2v_build_walk_edges (16-byte walk
+records), rdf2v_nonsink_starts (start set) and rdf2v_random_walks (every walk
+of every start entity, one launch). The default
 workload is the power-law graph with 1M entities, 200 predicates and 20M
 triples, depth 8, 50 walks per start entity (about 48.9M walks).
 
@@ -145,6 +146,7 @@ def main() -> int:
     row_ptr = torch.empty(V + 1, dtype=torch.int32, device=dev)
     edges = torch.empty((T, 2), dtype=torch.int32, device=dev)
     ws_build = torch.empty(max(rd.rdf2v_build_csr_workspace_size(T, V), 1), dtype=torch.uint8, device=dev)
+    walk_edges = torch.empty((T, 4), dtype=torch.int32, device=dev)
     ws_starts = torch.empty(rd.rdf2v_nonsink_starts_workspace_size(V), dtype=torch.uint8, device=dev)
     starts = torch.empty(V, dtype=torch.int32, device=dev)
     count = torch.empty(1, dtype=torch.int64, device=dev)
@@ -169,6 +171,7 @@ def main() -> int:
         e0.record(stream)
         csr = rd.rdf2v_build_csr(subj, pred, obj, V, P, workspace=ws_build, status=status,
                                  row_ptr=row_ptr, edges=edges, stream=stream)
+        csr = rd.rdf2v_build_walk_edges(csr, out=walk_edges, status=status, stream=stream)
         e1.record(stream)
         st, cnt = rd.rdf2v_nonsink_starts(csr, workspace=ws_starts, starts=starts, count=count,
                                           stream=stream, sync=False)

@@ -72,6 +72,13 @@ typedef struct rdf2v_csr {
   int64_t num_edges;
   const int32_t *row_ptr;
   const int32_t *edges;
+  /* Optional (may be NULL): the same out-edge records extended with the row
+   * bounds of their object, as written by rdf2v_build_walk_edges:
+   * walk_edges[num_edges][4] = (predicate, object, row_ptr[object],
+   * row_ptr[object + 1]), 16-byte aligned. When present, rdf2v_random_walks
+   * reads one 16-byte record per hop instead of a record plus the next
+   * entity's row bounds; the walks are identical either way. */
+  const int32_t *walk_edges;
 } rdf2v_csr;
 
 /*
@@ -102,6 +109,22 @@ rdf2v_status rdf2v_build_csr(const int32_t *subj, const int32_t *pred, const int
                              int64_t num_triples, int32_t num_entities, int32_t num_predicates,
                              int32_t *row_ptr_out, int32_t *edges_out, void *workspace,
                              size_t workspace_bytes, int32_t *status_dev, void *stream);
+
+/*
+ * Walk records: for every out-edge record k of the CSR,
+ *   walk_edges_out[k] = (edges[k][0], edges[k][1], row_ptr[o], row_ptr[o + 1])
+ * with o = edges[k][1], so that a walk learns the row of the entity it moves
+ * to from the record it has just read (one random access per hop; the walk
+ * definition is unchanged).
+ *
+ *   csr             CSR view (row_ptr and edges are read; walk_edges ignored).
+ *   walk_edges_out  [num_edges][4] int32 (device), written; 16-byte aligned.
+ *   status_dev      device int32 or NULL: RDF2V_STATUS_ID_OUT_OF_RANGE if an
+ *                   object id is out of range (its row bounds are written as
+ *                   0, 0).
+ */
+rdf2v_status rdf2v_build_walk_edges(const rdf2v_csr *csr, int32_t *walk_edges_out,
+                                    int32_t *status_dev, void *stream);
 
 /* Bytes of device workspace rdf2v_nonsink_starts needs. Pure host function. */
 size_t rdf2v_nonsink_starts_workspace_size(int32_t num_entities);
@@ -138,7 +161,9 @@ rdf2v_status rdf2v_nonsink_starts(const rdf2v_csr *csr, int32_t *starts_out, int
  * num_entities + p and x; e_{h+1} = x.
  *
  *   csr           view of a CSR as rdf2v_build_csr writes it (host pointer to
- *                 the struct; the arrays it points to are device memory).
+ *                 the struct; the arrays it points to are device memory). If
+ *                 csr->walk_edges is set it must hold rdf2v_build_walk_edges'
+ *                 records for this CSR; csr->edges is then not read.
  *   start_nodes   [num_start] int32 entity ids (device); duplicates and sinks
  *                 allowed.
  *   depth         hops per walk, 0 .. RDF2V_MAX_DEPTH.

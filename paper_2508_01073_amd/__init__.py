@@ -23,7 +23,8 @@ import torch
 
 __all__ = [
     "Csr", "Rdf2vError", "RDF2V_MAX_DEPTH", "RDF2V_STATUS_ID_OUT_OF_RANGE", "RDF2V_STATUS_BAD_CSR",
-    "rdf2v_build_csr_workspace_size", "rdf2v_build_csr", "rdf2v_nonsink_starts_workspace_size",
+    "rdf2v_build_csr_workspace_size", "rdf2v_build_csr", "rdf2v_build_walk_edges",
+    "rdf2v_nonsink_starts_workspace_size",
     "rdf2v_nonsink_starts", "rdf2v_random_walks", "rdf2v_status_string", "check_device_status",
     "library_path",
 ]
@@ -50,7 +51,7 @@ def library_path() -> str:
 class _CsrStruct(ctypes.Structure):
     _fields_ = [("num_entities", ctypes.c_int32), ("num_predicates", ctypes.c_int32),
                 ("num_edges", ctypes.c_int64), ("row_ptr", ctypes.c_void_p),
-                ("edges", ctypes.c_void_p)]
+                ("edges", ctypes.c_void_p), ("walk_edges", ctypes.c_void_p)]
 
 
 def _native():
@@ -67,6 +68,8 @@ def _native():
     lib.rdf2v_build_csr_workspace_size.restype = sz
     lib.rdf2v_build_csr.argtypes = [vp, vp, vp, i64, i32, i32, vp, vp, vp, sz, vp, vp]
     lib.rdf2v_build_csr.restype = ctypes.c_int
+    lib.rdf2v_build_walk_edges.argtypes = [csr_p, vp, vp, vp]
+    lib.rdf2v_build_walk_edges.restype = ctypes.c_int
     lib.rdf2v_nonsink_starts_workspace_size.argtypes = [i32]
     lib.rdf2v_nonsink_starts_workspace_size.restype = sz
     lib.rdf2v_nonsink_starts.argtypes = [csr_p, vp, vp, vp, sz, vp]
@@ -118,19 +121,24 @@ def _stream(device: torch.device, stream) -> ctypes.c_void_p:
 class Csr:
     """Subject-indexed CSR in device memory (see ``rdf2v_csr`` in rdf2v.h).
 
-    row_ptr: int32 [num_entities + 1]; edges: int32 [num_edges, 2] = (predicate, object)."""
+    row_ptr: int32 [num_entities + 1]; edges: int32 [num_edges, 2] = (predicate, object);
+    walk_edges (optional): int32 [num_edges, 4] = (predicate, object, row lo, row hi) of the
+    object, from rdf2v_build_walk_edges."""
     row_ptr: torch.Tensor
     edges: torch.Tensor
     num_entities: int
     num_predicates: int
+    walk_edges: torch.Tensor | None = None
 
     @property
     def num_edges(self) -> int:
         return int(self.edges.shape[0])
 
     def _c(self) -> _CsrStruct:
+        we = self.walk_edges
         return _CsrStruct(self.num_entities, self.num_predicates, self.num_edges,
-                          self.row_ptr.data_ptr(), self.edges.data_ptr() if self.edges.numel() else None)
+                          self.row_ptr.data_ptr(), self.edges.data_ptr() if self.edges.numel() else None,
+                          we.data_ptr() if we is not None and we.numel() else None)
 
 
 def rdf2v_build_csr_workspace_size(num_triples: int, num_entities: int) -> int:
@@ -160,6 +168,21 @@ def rdf2v_build_csr(subj: torch.Tensor, pred: torch.Tensor, obj: torch.Tensor, n
                               _stream(dev, stream))
     _check(st, "rdf2v_build_csr")
     return Csr(row_ptr, edges, num_entities, num_predicates)
+
+
+def rdf2v_build_walk_edges(csr: Csr, *, out: torch.Tensor | None = None,
+                           status: torch.Tensor | None = None, stream=None) -> Csr:
+    """Returns the Csr with walk_edges [num_edges, 4] = (predicate, object, row lo, row hi)
+    of the object, so the walks read one 16-byte record per hop."""
+    dev = csr.row_ptr.device
+    if out is None:
+        out = torch.empty((csr.num_edges, 4), dtype=torch.int32, device=dev)
+    if out.numel() < 4 * csr.num_edges:
+        raise ValueError("out too small for num_edges walk records")
+    c = csr._c()
+    st = _native().rdf2v_build_walk_edges(ctypes.byref(c), _ptr(out), _ptr(status), _stream(dev, stream))
+    _check(st, "rdf2v_build_walk_edges")
+    return Csr(csr.row_ptr, csr.edges, csr.num_entities, csr.num_predicates, out)
 
 
 def rdf2v_nonsink_starts_workspace_size(num_entities: int) -> int:

@@ -47,6 +47,21 @@ RDF2V_API rdf2v_status rdf2v_build_csr(const int32_t *subj, const int32_t *pred,
                                  static_cast<hipStream_t>(stream));
 }
 
+RDF2V_API rdf2v_status rdf2v_build_walk_edges(const rdf2v_csr *csr, int32_t *walk_edges_out,
+                                              int32_t *status_dev, void *stream) {
+  if (csr == nullptr || csr->row_ptr == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (csr->num_entities < 0 || csr->num_predicates < 0 || csr->num_edges < 0)
+    return RDF2V_ERR_INVALID_ARGUMENT;
+  if (csr->num_edges >= kInt32Limit || id_space_too_large(csr->num_entities, csr->num_predicates))
+    return RDF2V_ERR_TOO_LARGE;
+  if (csr->num_edges == 0) return RDF2V_OK;
+  if (csr->edges == nullptr || walk_edges_out == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if ((reinterpret_cast<uintptr_t>(csr->edges) & 7) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  if ((reinterpret_cast<uintptr_t>(walk_edges_out) & 15) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  return rdf2v::launch_walk_edges(csr->row_ptr, csr->edges, csr->num_edges, csr->num_entities,
+                                  walk_edges_out, status_dev, static_cast<hipStream_t>(stream));
+}
+
 RDF2V_API size_t rdf2v_nonsink_starts_workspace_size(int32_t num_entities) {
   return rdf2v::nonsink_workspace_bytes(num_entities);
 }
@@ -82,13 +97,18 @@ RDF2V_API rdf2v_status rdf2v_random_walks(const rdf2v_csr *csr, const int32_t *s
   if (walk_count == 0) return RDF2V_OK;
   if (start_nodes == nullptr || tokens_out == nullptr || len_out == nullptr || csr->row_ptr == nullptr)
     return RDF2V_ERR_INVALID_ARGUMENT;
-  if (csr->num_edges > 0 && csr->edges == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
-  if ((reinterpret_cast<uintptr_t>(csr->edges) & 7) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (csr->walk_edges != nullptr) {
+    if ((reinterpret_cast<uintptr_t>(csr->walk_edges) & 15) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  } else {
+    if (csr->num_edges > 0 && csr->edges == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+    if ((reinterpret_cast<uintptr_t>(csr->edges) & 7) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  }
   if (walk_count > INT64_MAX / (2 * int64_t(depth) + 1)) return RDF2V_ERR_TOO_LARGE;
 
   rdf2v::WalkArgs a;
   a.row_ptr = csr->row_ptr;
   a.edges = csr->edges;
+  a.walk_edges = csr->walk_edges;
   a.start = start_nodes;
   a.tokens = tokens_out;
   a.lens = len_out;

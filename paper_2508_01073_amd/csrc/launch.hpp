@@ -34,7 +34,8 @@ rdf2v_status launch_nonsink_starts(const int32_t *row_ptr, int32_t num_entities,
 
 struct WalkArgs {
   const int32_t *row_ptr;
-  const int32_t *edges;  // (predicate, object) pairs, 8-byte aligned
+  const int32_t *edges;       // (predicate, object) pairs, 8-byte aligned
+  const int32_t *walk_edges;  // optional (predicate, object, row lo, row hi), 16-byte aligned
   const int32_t *start;
   int32_t *tokens;
   int32_t *lens;
@@ -50,5 +51,9 @@ struct WalkArgs {
   uint32_t key_hi;
 };
 rdf2v_status launch_random_walks(const WalkArgs &args, hipStream_t stream);
+
+rdf2v_status launch_walk_edges(const int32_t *row_ptr, const int32_t *edges, int64_t num_edges,
+                               int32_t num_entities, int32_t *walk_edges_out, int32_t *status_dev,
+                               hipStream_t stream);
 
 }  // namespace rdf2v

@@ -3,10 +3,13 @@
 // One lane runs one walk (gpuRDF2vec Sec. 4.1 launches every walk of every
 // start entity at once instead of looping over entities; here the start of
 // walk w is start[w / walks_per_node], computed in the kernel, so nothing is
-// replicated in memory). Per hop a lane does two dependent gathers, the row
-// bounds of the current entity and then one (predicate, object) record, so the
-// kernel is bound by memory latency and random-access throughput; there is no
-// dense contraction and no use for MFMA.
+// replicated in memory). Each hop is a random gather whose address depends on
+// the previous one, and out-edge records are all about equally likely to be
+// read, so nearly every hop misses L2: the kernel is bound by the rate at which
+// the memory system serves L2-missing random reads. There is no dense
+// contraction and no use for MFMA. With walk records (predicate, object and
+// the object's row bounds in one 16-byte record) a hop is a single gather;
+// without them it is two (the record, then the next entity's row bounds).
 //
 // Layout choices for CDNA4:
 //  * one Philox4x32-10 block serves four consecutive hops of a walk, so the
@@ -60,7 +63,10 @@ __device__ __forceinline__ Words4 philox_block(uint32_t hop_block, uint64_t walk
   return {x0, x1, x2, x3};
 }
 
-template <int kBlock>
+// kFused: read (predicate, object, row lo, row hi) records, so each hop is one
+// 16-byte gather; otherwise read (predicate, object) and then the row bounds
+// of the object (two dependent gathers per hop).
+template <int kBlock, bool kFused>
 __global__ __launch_bounds__(kBlock) void random_walk_kernel(const WalkArgs a) {
   extern __shared__ __align__(16) int32_t tile[];
   const int width = 2 * a.depth + 1;
@@ -68,6 +74,7 @@ __global__ __launch_bounds__(kBlock) void random_walk_kernel(const WalkArgs a) {
   const int nrows = int(min(int64_t(kBlock), a.walk_count - row0));
   const int t = threadIdx.x;
   const int2 *__restrict__ edges = reinterpret_cast<const int2 *>(a.edges);
+  const v4i32 *__restrict__ walk_edges = reinterpret_cast<const v4i32 *>(a.walk_edges);
   const int32_t *__restrict__ row_ptr = a.row_ptr;
   const uint32_t V = uint32_t(a.num_entities);
   const uint32_t P = uint32_t(a.num_predicates);
@@ -83,16 +90,21 @@ __global__ __launch_bounds__(kBlock) void random_walk_kernel(const WalkArgs a) {
     len = 1;
     bool alive = uint32_t(e) < V;
     if (!alive) flags |= RDF2V_STATUS_ID_OUT_OF_RANGE;
+    int32_t lo = 0, hi = 0;
+    if (alive) {
+      lo = row_ptr[e];
+      hi = row_ptr[e + 1];
+    }
     for (int hb = 0; alive && hb < a.depth; hb += 4) {
-      const int32_t lo0 = row_ptr[e];
-      const int32_t hi0 = row_ptr[e + 1];
       const Words4 r = philox_block(uint32_t(hb >> 2), w, a.key_lo, a.key_hi);
       const uint32_t words[4] = {r.w0, r.w1, r.w2, r.w3};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         if (hb + j >= a.depth) break;
-        const int32_t lo = j == 0 ? lo0 : row_ptr[e];
-        const int32_t hi = j == 0 ? hi0 : row_ptr[e + 1];
+        if (!kFused && hb + j > 0) {
+          lo = row_ptr[e];
+          hi = row_ptr[e + 1];
+        }
         if (uint32_t(lo) > uint32_t(hi) || uint32_t(hi) > E) {
           flags |= RDF2V_STATUS_BAD_CSR;
           alive = false;
@@ -104,16 +116,27 @@ __global__ __launch_bounds__(kBlock) void random_walk_kernel(const WalkArgs a) {
           break;
         }
         const uint32_t k = __umulhi(words[j], deg);
-        const int2 rec = edges[uint32_t(lo) + k];
-        if (uint32_t(rec.x) >= P || uint32_t(rec.y) >= V) {
+        int32_t p, x;
+        if (kFused) {
+          const v4i32 rec = walk_edges[uint32_t(lo) + k];
+          p = rec.x;
+          x = rec.y;
+          lo = rec.z;
+          hi = rec.w;
+        } else {
+          const int2 rec = edges[uint32_t(lo) + k];
+          p = rec.x;
+          x = rec.y;
+        }
+        if (uint32_t(p) >= P || uint32_t(x) >= V) {
           flags |= RDF2V_STATUS_ID_OUT_OF_RANGE;
           alive = false;
           break;
         }
-        row[len] = int32_t(V) + rec.x;
-        row[len + 1] = rec.y;
+        row[len] = int32_t(V) + p;
+        row[len + 1] = x;
         len += 2;
-        e = rec.y;
+        e = x;
       }
     }
     for (int j = len; j < width; ++j) row[j] = -1;
@@ -136,21 +159,54 @@ __global__ __launch_bounds__(kBlock) void random_walk_kernel(const WalkArgs a) {
   if (flags != 0 && a.status != nullptr) atomicOr(a.status, flags);
 }
 
+// walk_edges[k] = (pred, obj, row_ptr[obj], row_ptr[obj + 1]) for record k.
+__global__ __launch_bounds__(256) void walk_edges_kernel(const int32_t *__restrict__ row_ptr,
+                                                         const int2 *__restrict__ edges, int64_t n,
+                                                         int32_t num_entities,
+                                                         v4i32 *__restrict__ out, int32_t *status) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= n) return;
+  const int2 r = edges[i];
+  int32_t lo = 0, hi = 0;
+  if (uint32_t(r.y) < uint32_t(num_entities)) {
+    lo = row_ptr[r.y];
+    hi = row_ptr[r.y + 1];
+  } else if (status != nullptr) {
+    atomicOr(status, RDF2V_STATUS_ID_OUT_OF_RANGE);
+  }
+  out[i] = v4i32{r.x, r.y, lo, hi};
+}
+
+template <int kBlock>
+rdf2v_status launch_walk_kernel(const WalkArgs &a, hipStream_t stream) {
+  const int width = 2 * a.depth + 1;
+  const int64_t blocks = (a.walk_count + kBlock - 1) / kBlock;
+  if (blocks >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
+  const size_t lds = size_t(kBlock) * width * 4;
+  if (a.walk_edges != nullptr)
+    random_walk_kernel<kBlock, true><<<dim3(unsigned(blocks)), dim3(kBlock), lds, stream>>>(a);
+  else
+    random_walk_kernel<kBlock, false><<<dim3(unsigned(blocks)), dim3(kBlock), lds, stream>>>(a);
+  RDF2V_LAUNCH_CHECK();
+  return RDF2V_OK;
+}
+
 }  // namespace
 
 rdf2v_status launch_random_walks(const WalkArgs &a, hipStream_t stream) {
-  const int width = 2 * a.depth + 1;
-  if (a.depth <= 16) {
-    constexpr int kBlock = 256;
-    const int64_t blocks = (a.walk_count + kBlock - 1) / kBlock;
-    if (blocks >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
-    random_walk_kernel<kBlock><<<dim3(unsigned(blocks)), dim3(kBlock), size_t(kBlock) * width * 4, stream>>>(a);
-  } else {
-    constexpr int kBlock = 64;
-    const int64_t blocks = (a.walk_count + kBlock - 1) / kBlock;
-    if (blocks >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
-    random_walk_kernel<kBlock><<<dim3(unsigned(blocks)), dim3(kBlock), size_t(kBlock) * width * 4, stream>>>(a);
-  }
+  // The LDS tile holds kBlock rows of 2*depth+1 tokens: 256 rows up to depth
+  // 16 (33.8 KB), 64 rows beyond (at most 33 KB at depth 64).
+  return a.depth <= 16 ? launch_walk_kernel<256>(a, stream) : launch_walk_kernel<64>(a, stream);
+}
+
+rdf2v_status launch_walk_edges(const int32_t *row_ptr, const int32_t *edges, int64_t num_edges,
+                               int32_t num_entities, int32_t *walk_edges_out, int32_t *status_dev,
+                               hipStream_t stream) {
+  if (num_edges == 0) return RDF2V_OK;
+  const int64_t blocks = (num_edges + 255) / 256;
+  walk_edges_kernel<<<dim3(unsigned(blocks)), dim3(256), 0, stream>>>(
+      row_ptr, reinterpret_cast<const int2 *>(edges), num_edges, num_entities,
+      reinterpret_cast<v4i32 *>(walk_edges_out), status_dev);
   RDF2V_LAUNCH_CHECK();
   return RDF2V_OK;
 }

@@ -30,13 +30,28 @@ def new_status() -> torch.Tensor:
     return torch.zeros(1, dtype=torch.int32, device=device())
 
 
-def gpu_csr(s, p, o, V, P, status=None) -> rd.Csr:
+def gpu_csr(s, p, o, V, P, status=None, walk_records=False) -> rd.Csr:
     st = new_status() if status is None else status
     csr = rd.rdf2v_build_csr(to_dev(s), to_dev(p), to_dev(o), V, P, status=st)
+    if walk_records:
+        csr = rd.rdf2v_build_walk_edges(csr, status=st)
     torch.cuda.synchronize()
     if status is None:
         rd.check_device_status(st, "rdf2v_build_csr")
     return csr
+
+
+def plain(csr: rd.Csr) -> rd.Csr:
+    """The same CSR without walk records (walks read the 8-byte records)."""
+    return rd.Csr(csr.row_ptr, csr.edges, csr.num_entities, csr.num_predicates, None)
+
+
+def assert_walk_records(csr: rd.Csr, rp_ref: np.ndarray, ed_ref: np.ndarray) -> None:
+    """walk_edges[k] = (predicate, object, row_ptr[object], row_ptr[object + 1])."""
+    we = csr.walk_edges.cpu().numpy().reshape(-1, 4)
+    o = ed_ref[:, 1].astype(np.int64)
+    expect = np.stack([ed_ref[:, 0], ed_ref[:, 1], rp_ref[o], rp_ref[o + 1]], axis=1)
+    assert np.array_equal(we, expect), "walk records differ from (p, o, row_ptr[o], row_ptr[o+1])"
 
 
 def gpu_walks(csr, starts_dev, wpn, depth, seed, walk_begin=0, walk_count=None, **kw):

@@ -30,7 +30,7 @@ def lib():
 
 def test_header_declares_the_calls():
     names = _declared_functions()
-    for n in ["rdf2v_build_csr", "rdf2v_build_csr_workspace_size", "rdf2v_random_walks",
+    for n in ["rdf2v_build_csr", "rdf2v_build_csr_workspace_size", "rdf2v_random_walks", "rdf2v_build_walk_edges",
               "rdf2v_nonsink_starts", "rdf2v_nonsink_starts_workspace_size", "rdf2v_status_string"]:
         assert n in names
 
@@ -132,6 +132,22 @@ def test_build_argument_validation(lib):
     assert f(FAKE, FAKE, FAKE, 100, 10, 3, FAKE, FAKE8, WS, ws - 1, None, None) == pkg.RDF2V_ERR_WORKSPACE
     assert f(FAKE, FAKE, FAKE, 100, 10, 3, FAKE, FAKE8, ctypes.c_void_p((1 << 41) + 64), ws, None, None) \
         == pkg.RDF2V_ERR_WORKSPACE
+
+
+def test_walk_edges_argument_validation(lib):
+    so, pkg = lib
+    f = so.rdf2v_build_walk_edges
+    E_INV = pkg.RDF2V_ERR_INVALID_ARGUMENT
+    assert f(None, FAKE, None, None) == E_INV
+    assert f(ctypes.byref(_csr(pkg, row_ptr=None)), FAKE, None, None) == E_INV
+    assert f(ctypes.byref(_csr(pkg)), None, None, None) == E_INV
+    assert f(ctypes.byref(_csr(pkg)), ctypes.c_void_p((1 << 40) + 8), None, None) == E_INV  # not 16-aligned
+    assert f(ctypes.byref(_csr(pkg, edges=None)), FAKE, None, None) == E_INV
+    assert f(ctypes.byref(_csr(pkg, E=2**31)), FAKE, None, None) == pkg.RDF2V_ERR_TOO_LARGE
+    assert f(ctypes.byref(_csr(pkg, E=0, edges=None)), None, None, None) == pkg.RDF2V_OK  # nothing to do
+    # walks reading walk records need them 16-byte aligned
+    c = pkg._CsrStruct(10, 3, 20, FAKE, FAKE8, ctypes.c_void_p((1 << 40) + 8))
+    assert _walk(lib, c) == E_INV
 
 
 def test_nonsink_argument_validation(lib):

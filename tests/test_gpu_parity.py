@@ -14,8 +14,8 @@ import torch
 import oracle
 import paper_2508_01073_amd as rd
 import synth
-from gpu_helpers import (assert_csr_equal, assert_rows_equal, check_walk_properties, compare_windows,
-                         device, gpu_csr, gpu_walks, new_status, say, to_dev)
+from gpu_helpers import (assert_csr_equal, assert_rows_equal, assert_walk_records, check_walk_properties,
+                         compare_windows, device, gpu_csr, gpu_walks, new_status, plain, say, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -49,13 +49,15 @@ def test_hand_graph_parity(name, depth):
     say(f"[hand] {name} depth={depth}")
     t = np.array(tr, dtype=np.int32)
     rp, ed = oracle.build_csr(t[:, 0], t[:, 1], t[:, 2], V, P)
-    csr = gpu_csr(t[:, 0], t[:, 1], t[:, 2], V, P)
+    csr = gpu_csr(t[:, 0], t[:, 1], t[:, 2], V, P, walk_records=True)
     assert_csr_equal(csr, rp, ed)
+    assert_walk_records(csr, rp, ed)
     wpn = 37
     for seed in (42, 2**63 + 5):
-        tok, ln = gpu_walks(csr, to_dev(starts), wpn, depth, seed)
         tr_, lr_ = oracle.random_walks(rp, ed, V, P, np.array(starts), wpn, depth, seed)
-        assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, f"{name} seed {seed}")
+        for c, what in [(csr, "walk records"), (plain(csr), "plain records")]:
+            tok, ln = gpu_walks(c, to_dev(starts), wpn, depth, seed)
+            assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, f"{name} seed {seed} {what}")
 
 
 # ----------------------------------------------------------------------------
@@ -77,16 +79,18 @@ def test_random_graph_parity(V, P, T):
     p = rng.integers(0, P, T).astype(np.int32)
     o = rng.integers(0, V, T).astype(np.int32)
     rp, ed = oracle.build_csr(s, p, o, V, P)
-    csr = gpu_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P, walk_records=True)
     assert_csr_equal(csr, rp, ed)
+    assert_walk_records(csr, rp, ed)
     starts = oracle.nonsink_starts(rp, V)
     starts_gpu = rd.rdf2v_nonsink_starts(csr)
     assert np.array_equal(starts_gpu.cpu().numpy(), starts)
     for depth, wpn in [(4, 3), (8, 2), (16, 1), (33, 1)]:
         sub = starts[:20_000]
-        tok, ln = gpu_walks(csr, to_dev(sub), wpn, depth, 42)
         tr_, lr_ = oracle.random_walks(rp, ed, V, P, sub, wpn, depth, 42)
-        assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, f"depth {depth}")
+        for c, what in [(csr, "walk records"), (plain(csr), "plain records")]:
+            tok, ln = gpu_walks(c, to_dev(sub), wpn, depth, 42)
+            assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, f"depth {depth} {what}")
 
 
 def test_powerlaw_small_with_sinks():
@@ -94,12 +98,14 @@ def test_powerlaw_small_with_sinks():
     V, P = 20_000, 40
     s, p, o = synth.powerlaw_triples(V, P, 300_000, sink_fraction=0.1)
     rp, ed = oracle.build_csr(s, p, o, V, P)
-    csr = gpu_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P, walk_records=True)
     assert_csr_equal(csr, rp, ed)
+    assert_walk_records(csr, rp, ed)
     starts = oracle.nonsink_starts(rp, V)
-    tok, ln = gpu_walks(csr, to_dev(starts), 3, 16, 7)
     tr_, lr_ = oracle.random_walks(rp, ed, V, P, starts, 3, 16, 7)
-    assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, "powerlaw small")
+    for c, what in [(csr, "walk records"), (plain(csr), "plain records")]:
+        tok, ln = gpu_walks(c, to_dev(starts), 3, 16, 7)
+        assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, f"powerlaw small {what}")
 
 
 # ----------------------------------------------------------------------------
@@ -112,14 +118,16 @@ def test_tiny_uniform_full_parity():
     s, p, o = synth.triples(w)
     V, P = w.num_entities, w.num_predicates
     rp, ed = oracle.build_csr(s, p, o, V, P)
-    csr = gpu_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P, walk_records=True)
     assert_csr_equal(csr, rp, ed)
+    assert_walk_records(csr, rp, ed)
     starts = oracle.nonsink_starts(rp, V)
     starts_dev = rd.rdf2v_nonsink_starts(csr)
     assert np.array_equal(starts_dev.cpu().numpy(), starts)
-    tok, ln = gpu_walks(csr, starts_dev, w.walks_per_node, w.depth, synth.WALK_SEED)
     tr_, lr_ = oracle.random_walks(rp, ed, V, P, starts, w.walks_per_node, w.depth, synth.WALK_SEED)
-    assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, "tiny_uniform")
+    for c, what in [(csr, "walk records"), (plain(csr), "plain records")]:
+        tok, ln = gpu_walks(c, starts_dev, w.walks_per_node, w.depth, synth.WALK_SEED)
+        assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, f"tiny_uniform {what}")
 
 
 def _windows(num_walks, wpn, starts, deg, rng, k=24, size=1024):
@@ -139,8 +147,9 @@ def test_full_size_workload(name):
     s, p, o = synth.triples(w)
     V, P = w.num_entities, w.num_predicates
     rp, ed = oracle.build_csr(s, p, o, V, P)
-    csr = gpu_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P, walk_records=True)
     assert_csr_equal(csr, rp, ed)
+    assert_walk_records(csr, rp, ed)
     starts = oracle.nonsink_starts(rp, V)
     starts_dev = rd.rdf2v_nonsink_starts(csr)
     assert np.array_equal(starts_dev.cpu().numpy(), starts)
@@ -149,9 +158,12 @@ def test_full_size_workload(name):
     tok, ln = gpu_walks(csr, starts_dev, w.walks_per_node, w.depth, synth.WALK_SEED)
     check_walk_properties(tok, ln, starts_dev, w.walks_per_node, V, P, w.depth)
     rng = np.random.default_rng(5)
-    n = compare_windows(csr, rp, ed, V, P, starts, w.walks_per_node, w.depth, synth.WALK_SEED, tok, ln,
-                        _windows(num_walks, w.walks_per_node, starts, np.diff(rp), rng))
+    win = _windows(num_walks, w.walks_per_node, starts, np.diff(rp), rng)
+    n = compare_windows(csr, rp, ed, V, P, starts, w.walks_per_node, w.depth, synth.WALK_SEED, tok, ln, win)
     say(f"[workload] {name}: {n} sampled rows bit-exact")
+    # the 8-byte-record path gives the same corpus
+    tok2, ln2 = gpu_walks(plain(csr), starts_dev, w.walks_per_node, w.depth, synth.WALK_SEED)
+    assert torch.equal(tok2, tok) and torch.equal(ln2, ln)
 
 
 # ----------------------------------------------------------------------------
@@ -162,7 +174,7 @@ def test_batches_concatenate_to_one_shot():
     say("[batches] uniform 50k entities")
     V, P = 50_000, 9
     s, p, o = synth.uniform_triples(V, P, 400_000)
-    csr = gpu_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P, walk_records=True)
     starts_dev = rd.rdf2v_nonsink_starts(csr)
     wpn, depth = 7, 6
     total = starts_dev.shape[0] * wpn
@@ -181,9 +193,10 @@ def test_repeat_runs_identical():
     say("[repeat] powerlaw 200k entities")
     V, P = 200_000, 30
     s, p, o = synth.powerlaw_triples(V, P, 3_000_000)
-    c1 = gpu_csr(s, p, o, V, P)
-    c2 = gpu_csr(s, p, o, V, P)
+    c1 = gpu_csr(s, p, o, V, P, walk_records=True)
+    c2 = gpu_csr(s, p, o, V, P, walk_records=True)
     assert torch.equal(c1.row_ptr, c2.row_ptr) and torch.equal(c1.edges, c2.edges)
+    assert torch.equal(c1.walk_edges, c2.walk_edges)
     st = rd.rdf2v_nonsink_starts(c1)
     a = gpu_walks(c1, st, 5, 8, 42)
     b = gpu_walks(c2, st, 5, 8, 42)
@@ -221,6 +234,15 @@ def test_inconsistent_csr_is_flagged_not_read():
         tok, ln = rd.rdf2v_random_walks(csr, to_dev([start]), 1, 4, 42, status=st)
         torch.cuda.synchronize()
         assert int(st.item()) & rd.RDF2V_STATUS_BAD_CSR
+    # walk records whose row bounds run past num_edges are caught the same way
+    good_rp = torch.tensor([0, 2, 3, 4, 4], dtype=torch.int32, device=dev)
+    recs = torch.tensor([[0, 1, 2, 9], [0, 2, 3, 9], [0, 1, 2, 9], [0, 3, 4, 4]], dtype=torch.int32,
+                        device=dev)
+    csr = rd.Csr(good_rp, edges, 4, 1, recs)
+    st = new_status()
+    rd.rdf2v_random_walks(csr, to_dev([0, 2]), 8, 6, 42, status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) & rd.RDF2V_STATUS_BAD_CSR
 
 
 def test_empty_and_degenerate_inputs():

@@ -19,8 +19,8 @@ import torch
 import oracle
 import paper_2508_01073_amd as rd
 import synth
-from gpu_helpers import (assert_csr_equal, check_walk_properties, compare_windows, gpu_csr, gpu_walks,
-                         say)
+from gpu_helpers import (assert_csr_equal, assert_walk_records, check_walk_properties, compare_windows,
+                         gpu_csr, gpu_walks, say)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -33,14 +33,15 @@ def test_wikidata_share_batched_parity():
     t0 = time.time()
     s, p, o = synth.triples(w)
     say(f"[wikidata share] generated in {time.time() - t0:.1f}s")
-    csr = gpu_csr(s, p, o, V, P)
-    say("[wikidata share] GPU CSR built")
+    csr = gpu_csr(s, p, o, V, P, walk_records=True)
+    say("[wikidata share] GPU CSR and walk records built")
     t0 = time.time()
     rp, ed = oracle.build_csr(s, p, o, V, P)
     say(f"[wikidata share] oracle CSR in {time.time() - t0:.1f}s")
     del s, p, o
     assert_csr_equal(csr, rp, ed)
-    say("[wikidata share] CSR bit-exact")
+    assert_walk_records(csr, rp, ed)
+    say("[wikidata share] CSR and walk records bit-exact")
     starts = oracle.nonsink_starts(rp, V)
     starts_dev = rd.rdf2v_nonsink_starts(csr)
     assert np.array_equal(starts_dev.cpu().numpy(), starts)
