@@ -26,14 +26,14 @@
 namespace rdf2v {
 namespace {
 
-constexpr int kSortThreads = 256;
-constexpr int kSortItems = 16;
+constexpr int kSortThreads = 512;
+constexpr int kSortItems = 8;
 constexpr int kTile = kSortThreads * kSortItems;     // triples per tile
 constexpr int kMaxDigitBits = 8;
 constexpr int kMaxBins = 1 << kMaxDigitBits;
-constexpr int kTileWaves = kSortThreads / kWave;     // 4
-constexpr int kWaveItems = kTile / kTileWaves;       // 1024 consecutive triples per wave
-constexpr int kRounds = kWaveItems / kWave;          // 16 rounds of 64
+constexpr int kTileWaves = kSortThreads / kWave;
+constexpr int kWaveItems = kTile / kTileWaves;       // consecutive triples per wave
+constexpr int kRounds = kWaveItems / kWave;          // rounds of 64 per wave
 
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 16;
@@ -44,29 +44,67 @@ static_assert(kMaxBins <= kSortThreads, "one thread per digit in the tile prefix
 // ---------------------------------------------------------------------------
 // Radix pass, step 1: per-tile digit histogram (+ id validation on pass 0).
 // ---------------------------------------------------------------------------
+// Each thread reads kSortItems keys as 16-byte vectors (all loads issued
+// before any histogram update) and counts them in its wave's own LDS
+// histogram, so lanes of different waves never contend for a bin.
 template <bool kValidate>
 __global__ __launch_bounds__(kSortThreads) void radix_count_kernel(
     const uint32_t *__restrict__ keys, const int32_t *__restrict__ pred,
     const int32_t *__restrict__ obj, int64_t n, int shift, int bits, int32_t num_entities,
     int32_t num_predicates, int32_t *__restrict__ counts, int64_t tiles, int32_t *status) {
-  __shared__ int hist[kMaxBins];
+  __shared__ int hist[kTileWaves][kMaxBins];
+  constexpr int kVec = 4;
+  constexpr int kLoads = kSortItems / kVec;
   const int bins = 1 << bits;
   const uint32_t mask = uint32_t(bins - 1);
-  for (int d = threadIdx.x; d < bins; d += kSortThreads) hist[d] = 0;
+  const int wave = threadIdx.x / kWave;
+  for (int i = threadIdx.x; i < kTileWaves * kMaxBins; i += kSortThreads) (&hist[0][0])[i] = 0;
   __syncthreads();
   const int64_t tile = blockIdx.x;
   const int64_t base = tile * kTile;
+  const uintptr_t addr_bits = reinterpret_cast<uintptr_t>(keys) |
+                              (kValidate ? (reinterpret_cast<uintptr_t>(pred) | reinterpret_cast<uintptr_t>(obj)) : 0);
+  const bool full = base + kTile <= n && (addr_bits & 15) == 0;
+  uint32_t k[kSortItems];
   int bad = 0;
-#pragma unroll 4
-  for (int i = 0; i < kSortItems; ++i) {
-    const int64_t idx = base + int64_t(i) * kSortThreads + threadIdx.x;
-    if (idx < n) {
-      const uint32_t k = keys[idx];
-      atomicAdd(&hist[(k >> shift) & mask], 1);
-      if (kValidate) {
-        bad |= k >= uint32_t(num_entities);
-        bad |= uint32_t(obj[idx]) >= uint32_t(num_entities);
-        bad |= uint32_t(pred[idx]) >= uint32_t(num_predicates);
+  if (full) {
+    // 16-byte loads: vector v of the tile holds keys 4v .. 4v+3.
+    const uint4 *k4 = reinterpret_cast<const uint4 *>(keys + base);
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const uint4 v = k4[i * kSortThreads + threadIdx.x];
+      k[kVec * i + 0] = v.x; k[kVec * i + 1] = v.y; k[kVec * i + 2] = v.z; k[kVec * i + 3] = v.w;
+    }
+    if (kValidate) {
+      const int4 *p4 = reinterpret_cast<const int4 *>(pred + base);
+      const int4 *o4 = reinterpret_cast<const int4 *>(obj + base);
+#pragma unroll
+      for (int i = 0; i < kLoads; ++i) {
+        const int4 pv = p4[i * kSortThreads + threadIdx.x];
+        const int4 ov = o4[i * kSortThreads + threadIdx.x];
+        bad |= (uint32_t(pv.x) >= uint32_t(num_predicates)) | (uint32_t(pv.y) >= uint32_t(num_predicates)) |
+               (uint32_t(pv.z) >= uint32_t(num_predicates)) | (uint32_t(pv.w) >= uint32_t(num_predicates));
+        bad |= (uint32_t(ov.x) >= uint32_t(num_entities)) | (uint32_t(ov.y) >= uint32_t(num_entities)) |
+               (uint32_t(ov.z) >= uint32_t(num_entities)) | (uint32_t(ov.w) >= uint32_t(num_entities));
+      }
+#pragma unroll
+      for (int i = 0; i < kSortItems; ++i) bad |= k[i] >= uint32_t(num_entities);
+    }
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) atomicAdd(&hist[wave][(k[i] >> shift) & mask], 1);
+  } else {
+    // ragged last tile or unaligned input: scalar loads of the same items
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+      const int64_t idx = base + int64_t(i / kVec) * (kSortThreads * kVec) + threadIdx.x * kVec + (i % kVec);
+      if (idx < n) {
+        const uint32_t key = keys[idx];
+        atomicAdd(&hist[wave][(key >> shift) & mask], 1);
+        if (kValidate) {
+          bad |= key >= uint32_t(num_entities);
+          bad |= uint32_t(obj[idx]) >= uint32_t(num_entities);
+          bad |= uint32_t(pred[idx]) >= uint32_t(num_predicates);
+        }
       }
     }
   }
@@ -76,7 +114,12 @@ __global__ __launch_bounds__(kSortThreads) void radix_count_kernel(
   } else {
     __syncthreads();
   }
-  for (int d = threadIdx.x; d < bins; d += kSortThreads) counts[int64_t(d) * tiles + tile] = hist[d];
+  for (int d = threadIdx.x; d < bins; d += kSortThreads) {
+    int c = 0;
+#pragma unroll
+    for (int w = 0; w < kTileWaves; ++w) c += hist[w][d];
+    counts[int64_t(d) * tiles + tile] = c;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -105,7 +148,7 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
   for (int i = threadIdx.x; i < kTileWaves * kMaxBins; i += kSortThreads) (&wave_count[0][0])[i] = 0;
   __syncthreads();
 
-  // Wave `wave` owns tile items [wave*1024, wave*1024+1024), visited in order.
+  // Wave `wave` owns tile items [wave*kWaveItems, (wave+1)*kWaveItems), visited in order.
   uint32_t key[kRounds];
   int2 pay[kRounds];
   int rank[kRounds];

@@ -30,6 +30,7 @@ namespace rdf2v {
 namespace {
 
 typedef int32_t v4i32 __attribute__((ext_vector_type(4)));
+typedef int32_t v2i32 __attribute__((ext_vector_type(2)));
 
 // Philox4x32-10 (Salmon, Moraes, Dror & Shaw, SC'11): ten rounds of two
 // 32x32->64-bit products of counter words 0 and 2 with the Philox multipliers,
@@ -160,21 +161,47 @@ __global__ __launch_bounds__(kBlock) void random_walk_kernel(const WalkArgs a) {
 }
 
 // walk_edges[k] = (pred, obj, row_ptr[obj], row_ptr[obj + 1]) for record k.
-__global__ __launch_bounds__(256) void walk_edges_kernel(const int32_t *__restrict__ row_ptr,
-                                                         const int2 *__restrict__ edges, int64_t n,
-                                                         int32_t num_entities,
-                                                         v4i32 *__restrict__ out, int32_t *status) {
-  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (i >= n) return;
-  const int2 r = edges[i];
-  int32_t lo = 0, hi = 0;
-  if (uint32_t(r.y) < uint32_t(num_entities)) {
-    lo = row_ptr[r.y];
-    hi = row_ptr[r.y + 1];
-  } else if (status != nullptr) {
-    atomicOr(status, RDF2V_STATUS_ID_OUT_OF_RANGE);
+// Each thread handles kWalkEdgeItems records strided by the block size, issuing
+// all loads, then all row-bound gathers, then all stores, so that several
+// independent memory operations per lane are in flight.
+constexpr int kWalkEdgeThreads = 256;
+constexpr int kWalkEdgeItems = 4;
+constexpr int kWalkEdgeTile = kWalkEdgeThreads * kWalkEdgeItems;
+
+__global__ __launch_bounds__(kWalkEdgeThreads) void walk_edges_kernel(
+    const int32_t *__restrict__ row_ptr, const int2 *__restrict__ edges, int64_t n,
+    int32_t num_entities, v4i32 *__restrict__ out, int32_t *status) {
+  const int64_t base = int64_t(blockIdx.x) * kWalkEdgeTile + threadIdx.x;
+  int2 rec[kWalkEdgeItems];
+  int2 bounds[kWalkEdgeItems];
+  int bad = 0;
+#pragma unroll
+  for (int j = 0; j < kWalkEdgeItems; ++j) {
+    const int64_t i = base + j * kWalkEdgeThreads;
+    rec[j] = make_int2(0, 0);
+    if (i < n) {
+      // streamed once: non-temporal, so the row_ptr lines gathered below stay in L2
+      const v2i32 v = __builtin_nontemporal_load(reinterpret_cast<const v2i32 *>(edges) + i);
+      rec[j] = make_int2(v.x, v.y);
+    }
   }
-  out[i] = v4i32{r.x, r.y, lo, hi};
+#pragma unroll
+  for (int j = 0; j < kWalkEdgeItems; ++j) {
+    const int64_t i = base + j * kWalkEdgeThreads;
+    bounds[j] = make_int2(0, 0);
+    if (i < n) {
+      if (uint32_t(rec[j].y) < uint32_t(num_entities))
+        bounds[j] = make_int2(row_ptr[rec[j].y], row_ptr[rec[j].y + 1]);
+      else
+        bad = 1;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kWalkEdgeItems; ++j) {
+    const int64_t i = base + j * kWalkEdgeThreads;
+    if (i < n) __builtin_nontemporal_store(v4i32{rec[j].x, rec[j].y, bounds[j].x, bounds[j].y}, out + i);
+  }
+  if (bad && status != nullptr) atomicOr(status, RDF2V_STATUS_ID_OUT_OF_RANGE);
 }
 
 template <int kBlock>
@@ -203,8 +230,8 @@ rdf2v_status launch_walk_edges(const int32_t *row_ptr, const int32_t *edges, int
                                int32_t num_entities, int32_t *walk_edges_out, int32_t *status_dev,
                                hipStream_t stream) {
   if (num_edges == 0) return RDF2V_OK;
-  const int64_t blocks = (num_edges + 255) / 256;
-  walk_edges_kernel<<<dim3(unsigned(blocks)), dim3(256), 0, stream>>>(
+  const int64_t blocks = (num_edges + kWalkEdgeTile - 1) / kWalkEdgeTile;
+  walk_edges_kernel<<<dim3(unsigned(blocks)), dim3(kWalkEdgeThreads), 0, stream>>>(
       row_ptr, reinterpret_cast<const int2 *>(edges), num_edges, num_entities,
       reinterpret_cast<v4i32 *>(walk_edges_out), status_dev);
   RDF2V_LAUNCH_CHECK();
