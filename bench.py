@@ -60,7 +60,7 @@ def useful_bytes(lens, depth: int, num_start: int) -> tuple[int, int, int]:
     return gathered + written, hops, tokens
 
 
-def traffic_from_profile(num_walks: int):
+def traffic_from_profile(workload: str, num_walks: int):
     """HBM bytes per walk launch from the committed rocprofv3 --pmc summary, scaled by
     the copy-kernel calibration recorded there; None when absent or taken from other
     kernel sources or another launch size."""
@@ -69,7 +69,8 @@ def traffic_from_profile(num_walks: int):
             pmc = json.load(fh)
     except (OSError, ValueError):
         return None
-    if pmc.get("kernel_source_hash") != kernel_source_hash() or pmc.get("num_walks") != num_walks:
+    if (pmc.get("kernel_source_hash") != kernel_source_hash() or pmc.get("num_walks") != num_walks
+            or pmc.get("workload") != workload):
         return None
     return pmc.get("hbm_bytes_per_launch")
 
@@ -154,8 +155,11 @@ def main() -> int:
     status = torch.zeros(1, dtype=torch.int32, device=dev)
     max_walks = V * wpn
     width = 2 * d + 1
-    tokens = torch.empty((max_walks, width), dtype=torch.int32, device=dev)
-    lens = torch.empty(max_walks, dtype=torch.int32, device=dev)
+    # Walks are produced in batches of w.batch_walks into one reused buffer when the
+    # workload asks for it (the 500M-triple share); otherwise in one launch.
+    batch_cap = min(max_walks, w.batch_walks) if w.batch_walks else max_walks
+    tokens = torch.empty((batch_cap, width), dtype=torch.int32, device=dev)
+    lens = torch.empty(batch_cap, dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream(dev)
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
@@ -175,7 +179,7 @@ def main() -> int:
     copy_gbs = 3 * 2 * (copy_mib << 20) / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del a, b
 
-    def step(record):
+    def step(record, measure=None):
         e0, e1, e2, e3 = ev(), ev(), ev(), ev()
         e0.record(stream)
         csr = rd.rdf2v_build_csr(subj, pred, obj, V, P, workspace=ws_build, status=status,
@@ -187,19 +191,30 @@ def main() -> int:
         n_start = int(cnt.item())
         e2.record(stream)
         n_walks = n_start * wpn
-        rd.rdf2v_random_walks(csr, st[:n_start], wpn, d, 42, 0, n_walks, tokens=tokens[:n_walks],
-                              lens=lens[:n_walks], status=status, stream=stream)
+        launches = 0
+        for b0 in range(0, n_walks, batch_cap):
+            c = min(batch_cap, n_walks - b0)
+            rd.rdf2v_random_walks(csr, st[:n_start], wpn, d, 42, b0, c, tokens=tokens[:c],
+                                  lens=lens[:c], status=status, stream=stream)
+            launches += 1
+            if measure is not None:
+                starts_read = (b0 + c + wpn - 1) // wpn - b0 // wpn
+                measure.append(useful_bytes(lens[:c], d, starts_read))
         e3.record(stream)
-        record.append((e0, e1, e2, e3, n_start))
+        record.append((e0, e1, e2, e3, n_start, launches))
 
     warm = []
-    for _ in range(max(args.warmup, 1)):
+    for _ in range(max(args.warmup, 1) - 1):
         step(warm)
+    per_batch = []
+    step(warm, measure=per_batch)  # the last warm-up step also measures the useful bytes
     torch.cuda.synchronize()
     rd.check_device_status(status, "warmup")
-    n_start = warm[-1][4]
+    n_start, launches = warm[-1][4], warm[-1][5]
     n_walks = n_start * wpn
-    ub, hops, ntok = useful_bytes(lens[:n_walks], d, n_start)
+    ub = sum(x[0] for x in per_batch)
+    hops = sum(x[1] for x in per_batch)
+    ntok = sum(x[2] for x in per_batch)
 
     rec = []
     torch.cuda.synchronize()
@@ -212,11 +227,11 @@ def main() -> int:
 
     elapsed = t1 - t0
     ms_step = 1e3 * elapsed / args.steps
-    build_ms = float(np.mean([a.elapsed_time(b) for a, b, _, _, _ in rec]))
-    starts_ms = float(np.mean([b.elapsed_time(c) for _, b, c, _, _ in rec]))
-    walk_ms = float(np.mean([c.elapsed_time(e) for _, _, c, e, _ in rec]))
+    build_ms = float(np.mean([r[0].elapsed_time(r[1]) for r in rec]))
+    starts_ms = float(np.mean([r[1].elapsed_time(r[2]) for r in rec]))
+    walk_ms = float(np.mean([r[2].elapsed_time(r[3]) for r in rec]))  # all walk launches of a step
     achieved = ub / (walk_ms * 1e-3) / 1e9
-    traffic = traffic_from_profile(n_walks)
+    traffic = traffic_from_profile(w.name, n_walks) if launches == 1 else None
 
     out = {
         "metric": METRIC,
@@ -234,7 +249,7 @@ def main() -> int:
         "config": {
             "workload": w.name, "num_entities": V, "num_predicates": P, "num_triples": T,
             "graph": w.kind, "depth": d, "walks_per_node": wpn, "num_start": n_start,
-            "num_walks": n_walks, "seed": 42,
+            "num_walks": n_walks, "seed": 42, "batch_walks": batch_cap if launches > 1 else None,
         },
         "roofline": {
             "kernel": "random_walk_kernel",
@@ -244,7 +259,9 @@ def main() -> int:
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": traffic,
-            "useful_bytes_per_launch": ub,
+            "useful_bytes_per_launch": ub if launches == 1 else None,
+            "useful_bytes_per_step": ub,
+            "launches_per_step": launches,
         },
         "copy_reference_GBps": copy_gbs,
         "walk_kernel_ms": walk_ms,
