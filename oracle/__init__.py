@@ -67,6 +67,9 @@ def _load():
                                            ctypes.c_int32, ctypes.c_uint64, ctypes.c_int64,
                                            ctypes.c_int64, i32p, i32p]
     lib.rdf2v_ref_random_walks.restype = ctypes.c_int
+    lib.rdf2v_ref_skipgram_pairs.argtypes = [i32p, i32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                             i32p, ctypes.c_int64]
+    lib.rdf2v_ref_skipgram_pairs.restype = ctypes.c_int64
     _lib = lib
     return lib
 
@@ -158,3 +161,18 @@ def random_walks(row_ptr, edges, num_entities: int, num_predicates: int, start_n
     if status != OK:
         raise OracleError(status, "rdf2v_ref_random_walks")
     return tokens, lens
+
+
+def skipgram_pairs(tokens, lens, window: int) -> np.ndarray:
+    """(center, context) pairs [N, 2] of walk rows tokens[W, width] with lens[W] valid tokens:
+    every context within `window` positions of its center, in order walk, center, context."""
+    lib = _load()
+    tok = _i32(tokens)
+    ln = _i32(lens)
+    w, width = (tok.shape[0], tok.shape[1]) if tok.ndim == 2 else (ln.shape[0], 1)
+    n = lib.rdf2v_ref_skipgram_pairs(_ptr(tok), _ptr(ln), w, width, window, None, 0)
+    if n < 0:
+        raise OracleError(int(-n), "rdf2v_ref_skipgram_pairs")
+    pairs = np.empty((n, 2), dtype=np.int32)
+    lib.rdf2v_ref_skipgram_pairs(_ptr(tok), _ptr(ln), w, width, window, _ptr(pairs), n)
+    return pairs

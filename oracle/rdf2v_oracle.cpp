@@ -218,4 +218,33 @@ int rdf2v_ref_random_walks(const int32_t *row_ptr, const int32_t *edges, int32_t
   return REF_OK;
 }
 
+// Skip-gram training pairs (Sec. 3.2: the data module turns the walk corpus
+// into center-context pairs; Sec. 3.1: padding is dropped first). For walk r
+// with L = len[r] valid tokens t_0 .. t_{L-1}, every center position i and
+// every context position j with 1 <= |i - j| <= window and 0 <= j < L give the
+// pair (t_i, t_j), in the order walk, then i, then j. Returns the number of
+// pairs; writes at most `capacity` of them to pairs[][2]. A negative return is
+// an argument error.
+int64_t rdf2v_ref_skipgram_pairs(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                 int32_t row_width, int32_t window, int32_t *pairs, int64_t capacity) {
+  if (num_walks < 0 || row_width < 1 || window < 0 || capacity < 0) return -REF_ERR_INVALID_ARGUMENT;
+  int64_t n = 0;
+  for (int64_t r = 0; r < num_walks; ++r) {
+    const int32_t *row = tokens + r * row_width;
+    const int64_t L = len[r];
+    if (L < 0 || L > row_width) return -REF_ERR_INVALID_ARGUMENT;
+    for (int64_t i = 0; i < L; ++i) {
+      for (int64_t j = i - window; j <= i + window; ++j) {
+        if (j == i || j < 0 || j >= L) continue;
+        if (n < capacity) {
+          pairs[2 * n + 0] = row[i];
+          pairs[2 * n + 1] = row[j];
+        }
+        ++n;
+      }
+    }
+  }
+  return n;
+}
+
 }  // extern "C"

@@ -279,3 +279,50 @@ def test_unaligned_output_rows():
     tr_, lr_ = oracle.random_walks(rp, ed, V, P, starts, wpn, depth, 42)
     assert_rows_equal(tok.cpu().numpy(), lens.cpu().numpy(), tr_, lr_, "unaligned")
     assert int(buf[0].item()) == 7
+
+
+def test_walk_ids_beyond_2_pow_32():
+    say("[edge] walk ids >= 2^32 (Philox counter high word)")
+    V, P = 5000, 7
+    s, p, o = synth.uniform_triples(V, P, 40_000)
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P, walk_records=True)
+    starts = oracle.nonsink_starts(rp, V)[:3]
+    wpn = 2**31 - 1                      # 3 * wpn walks > 2^32
+    for b in (2**32 - 700, 2**32 + 5, 3 * wpn - 1000):
+        tr_, lr_ = oracle.random_walks(rp, ed, V, P, starts, wpn, 9, 42, b, 1000)
+        for c, what in [(csr, "walk records"), (plain(csr), "plain records")]:
+            tok, ln = gpu_walks(c, to_dev(starts), wpn, 9, 42, b, 1000)
+            assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, f"walks from {b} {what}")
+
+
+def test_concurrent_streams_do_not_interfere():
+    say("[streams] two graphs built and walked on two streams at once")
+    dev = device()
+    graphs = [synth.uniform_triples(30_000, 9, 300_000, seed=1), synth.powerlaw_triples(40_000, 11, 400_000, seed=2)]
+    sizes = [(30_000, 9), (40_000, 11)]
+    streams = [torch.cuda.Stream(dev), torch.cuda.Stream(dev)]
+    inputs = [[to_dev(a) for a in g] for g in graphs]
+    torch.cuda.synchronize()
+    results = []
+    for (sd, pd, od), (V, P), strm in zip(inputs, sizes, streams):
+        with torch.cuda.stream(strm):
+            st = torch.zeros(1, dtype=torch.int32, device=dev)
+            csr = rd.rdf2v_build_csr(sd, pd, od, V, P, status=st, stream=strm)
+            csr = rd.rdf2v_build_walk_edges(csr, status=st, stream=strm)
+            starts, cnt = rd.rdf2v_nonsink_starts(csr, stream=strm, sync=False)
+            results.append((csr, starts, cnt, st, strm))
+    outs = []
+    for csr, starts, cnt, st, strm in results:
+        strm.synchronize()
+        n = int(cnt.item())
+        with torch.cuda.stream(strm):
+            outs.append(rd.rdf2v_random_walks(csr, starts[:n], 4, 6, 42, status=st, stream=strm))
+    torch.cuda.synchronize()
+    for (s, p, o), (V, P), (csr, starts, cnt, st, _), (tok, ln) in zip(graphs, sizes, results, outs):
+        rd.check_device_status(st, "concurrent")
+        rp, ed = oracle.build_csr(s, p, o, V, P)
+        assert_csr_equal(csr, rp, ed)
+        st_ref = oracle.nonsink_starts(rp, V)
+        tr_, lr_ = oracle.random_walks(rp, ed, V, P, st_ref, 4, 6, 42)
+        assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, f"stream graph V={V}")
