@@ -108,6 +108,47 @@ def cpu_baseline(w, s, p, o, target_seconds: float):
     }
 
 
+def time_pairs(rd, torch, tokens, lens, n_walks, batch_cap, width, window, pair_batch, stream, ev):
+    """Time rdf2v_skipgram_pairs over the walk rows left in the output buffer (the whole corpus
+    when it was produced in one launch), in batches of `pair_batch` walks.
+
+    Algorithmic bytes: each walk row and its length are read once (4 * width + 4 B) and every
+    pair is written once (8 B)."""
+    dev = tokens.device
+    rows = min(n_walks, batch_cap)
+    pair_batch = min(pair_batch, rows)
+    # the largest batch bounds the pair count: 2 * window * width pairs per walk at most
+    cap = pair_batch * 2 * min(window, width) * width
+    pairs = torch.empty((cap, 2), dtype=torch.int32, device=dev)
+    ws = torch.empty(rd.rdf2v_skipgram_pairs_workspace_size(pair_batch), dtype=torch.uint8, device=dev)
+    count = torch.empty(1, dtype=torch.int64, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    total_pairs = 0
+    for b0 in range(0, rows, pair_batch):  # warm-up pass that also counts
+        c = min(pair_batch, rows - b0)
+        rd.rdf2v_skipgram_pairs(tokens[b0:b0 + c], lens[b0:b0 + c], window, pairs=pairs, count=count,
+                                workspace=ws, status=status, stream=stream)
+        torch.cuda.synchronize()
+        total_pairs += int(count.item())
+    rd.check_device_status(status, "skipgram pairs")
+    e0, e1 = ev(), ev()
+    e0.record(stream)
+    for b0 in range(0, rows, pair_batch):
+        c = min(pair_batch, rows - b0)
+        rd.rdf2v_skipgram_pairs(tokens[b0:b0 + c], lens[b0:b0 + c], window, pairs=pairs, count=count,
+                                workspace=ws, status=status, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    useful = rows * (4 * width + 4) + 8 * total_pairs
+    return {
+        "window": window, "walks": rows, "pairs": total_pairs, "batch_walks": pair_batch,
+        "ms": ms, "pairs_per_s": total_pairs / (ms * 1e-3),
+        "useful_bytes": useful, "achieved_GBps": useful / (ms * 1e-3) / 1e9,
+        "frac_of_hbm_peak": useful / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -116,6 +157,10 @@ def main() -> int:
     ap.add_argument("--workload", default="powerlaw_20m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--pairs-window", type=int, default=0,
+                    help="also time skip-gram pair generation over the corpus with this window "
+                         "(0: off)")
+    ap.add_argument("--pairs-batch-walks", type=int, default=8_000_000)
     ap.add_argument("--copy-probe-mib", type=int, default=1024,
                     help="size of the plain device copy timed first (bandwidth reference, "
                          "counter calibration)")
@@ -273,6 +318,9 @@ def main() -> int:
         "walk_kernel_hops_per_s": hops / (walk_ms * 1e-3),
         "padded_token_slots_per_s": n_walks * width / (walk_ms * 1e-3),
     }
+    if args.pairs_window > 0:
+        out["skipgram_pairs"] = time_pairs(rd, torch, tokens, lens, n_walks, batch_cap, width,
+                                           args.pairs_window, args.pairs_batch_walks, stream, ev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, s, p, o, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -52,6 +52,8 @@ typedef enum rdf2v_status {
 /* Bits ORed into *status_dev by the kernels. */
 #define RDF2V_STATUS_ID_OUT_OF_RANGE 0x1 /* a subject/object/start id >= num_entities or < 0, or a predicate id out of range */
 #define RDF2V_STATUS_BAD_CSR 0x2         /* row_ptr not non-decreasing within [0, num_edges] */
+#define RDF2V_STATUS_BAD_LENGTH 0x4      /* a walk length outside [0, row_width] (treated as clamped) */
+#define RDF2V_STATUS_CAPACITY 0x8        /* more pairs than the output holds (the rest are not written) */
 
 /* Longest walk, in hops. A walk row holds 2 * depth + 1 tokens. */
 #define RDF2V_MAX_DEPTH 64
@@ -179,6 +181,39 @@ rdf2v_status rdf2v_random_walks(const rdf2v_csr *csr, const int32_t *start_nodes
                                 int32_t walks_per_node, int32_t depth, uint64_t seed,
                                 int64_t walk_begin, int64_t walk_count, int32_t *tokens_out,
                                 int32_t *len_out, int32_t *status_dev, void *stream);
+
+/* Bytes of device workspace rdf2v_skipgram_pairs needs. Pure host function. */
+size_t rdf2v_skipgram_pairs_workspace_size(int64_t num_walks);
+
+/*
+ * Skip-gram training pairs from walk rows (gpuRDF2vec Sec. 3.2: the data
+ * module turns the walk corpus into center-context pairs; Sec. 3.1: the -1
+ * padding is dropped first).
+ *
+ * For walk r with L = len[r] valid tokens t_0 .. t_{L-1}, every center
+ * position i and every context position j with 1 <= |i - j| <= window and
+ * 0 <= j < L give the pair (t_i, t_j); pairs are ordered by walk, then i, then
+ * j. A walk of L tokens gives 2 * sum_{d=1}^{min(window, L-1)} (L - d) pairs.
+ *
+ *   tokens          [num_walks][row_width] int32 walk rows (device), as
+ *                   rdf2v_random_walks writes them.
+ *   len             [num_walks] int32 valid tokens per row (device).
+ *   row_width       1 .. 2 * RDF2V_MAX_DEPTH + 1.
+ *   window          >= 0 (the paper's example uses 5).
+ *   pairs_out       [pair_capacity][2] int32 (center, context) (device); may
+ *                   be NULL when pair_capacity == 0 (count only).
+ *   pair_count_out  one int64 in device memory: the total number of pairs,
+ *                   also when it exceeds pair_capacity (then only the first
+ *                   pair_capacity pairs are written and RDF2V_STATUS_CAPACITY
+ *                   is raised).
+ *   workspace       device scratch, rdf2v_skipgram_pairs_workspace_size()
+ *                   bytes, 256-byte aligned.
+ *   status_dev      device int32 or NULL.
+ */
+rdf2v_status rdf2v_skipgram_pairs(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                  int32_t row_width, int32_t window, int32_t *pairs_out,
+                                  int64_t pair_capacity, int64_t *pair_count_out, void *workspace,
+                                  size_t workspace_bytes, int32_t *status_dev, void *stream);
 
 /* Static, human-readable name of a status code. */
 const char *rdf2v_status_string(rdf2v_status status);

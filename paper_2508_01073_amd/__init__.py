@@ -25,7 +25,8 @@ __all__ = [
     "Csr", "Rdf2vError", "RDF2V_MAX_DEPTH", "RDF2V_STATUS_ID_OUT_OF_RANGE", "RDF2V_STATUS_BAD_CSR",
     "rdf2v_build_csr_workspace_size", "rdf2v_build_csr", "rdf2v_build_walk_edges",
     "rdf2v_nonsink_starts_workspace_size",
-    "rdf2v_nonsink_starts", "rdf2v_random_walks", "rdf2v_status_string", "check_device_status",
+    "rdf2v_nonsink_starts", "rdf2v_random_walks", "rdf2v_skipgram_pairs_workspace_size",
+    "rdf2v_skipgram_pairs", "rdf2v_status_string", "check_device_status",
     "library_path",
 ]
 
@@ -39,6 +40,8 @@ RDF2V_ERR_WORKSPACE = 4
 RDF2V_ERR_HIP = 5
 RDF2V_STATUS_ID_OUT_OF_RANGE = 0x1
 RDF2V_STATUS_BAD_CSR = 0x2
+RDF2V_STATUS_BAD_LENGTH = 0x4
+RDF2V_STATUS_CAPACITY = 0x8
 RDF2V_MAX_DEPTH = 64
 
 _lib = None
@@ -76,6 +79,10 @@ def _native():
     lib.rdf2v_nonsink_starts.restype = ctypes.c_int
     lib.rdf2v_random_walks.argtypes = [csr_p, vp, i64, i32, i32, u64, i64, i64, vp, vp, vp, vp]
     lib.rdf2v_random_walks.restype = ctypes.c_int
+    lib.rdf2v_skipgram_pairs_workspace_size.argtypes = [i64]
+    lib.rdf2v_skipgram_pairs_workspace_size.restype = sz
+    lib.rdf2v_skipgram_pairs.argtypes = [vp, vp, i64, i32, i32, vp, i64, vp, vp, sz, vp, vp]
+    lib.rdf2v_skipgram_pairs.restype = ctypes.c_int
     lib.rdf2v_status_string.argtypes = [ctypes.c_int]
     lib.rdf2v_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -238,10 +245,49 @@ def rdf2v_random_walks(csr: Csr, start_nodes: torch.Tensor, walks_per_node: int,
     return tokens, lens
 
 
+def rdf2v_skipgram_pairs_workspace_size(num_walks: int) -> int:
+    return int(_native().rdf2v_skipgram_pairs_workspace_size(num_walks))
+
+
+def rdf2v_skipgram_pairs(tokens: torch.Tensor, lens: torch.Tensor, window: int, *,
+                         pairs: torch.Tensor | None = None, count: torch.Tensor | None = None,
+                         workspace: torch.Tensor | None = None, status: torch.Tensor | None = None,
+                         stream=None):
+    """Walk rows tokens [W, width] + lens [W] -> (center, context) pairs [N, 2] int32.
+
+    With `pairs` given, writes at most pairs.shape[0] pairs and returns (pairs, count) with the
+    device int64 total (no host synchronisation). Without it, a first call counts, the host reads
+    the count, and a second call fills a tensor of exactly that size, which is returned."""
+    _dev_i32(tokens, "tokens"); _dev_i32(lens, "lens")
+    dev = tokens.device
+    w = int(lens.shape[0])
+    width = int(tokens.shape[1]) if tokens.dim() == 2 else 1
+    if workspace is None:
+        workspace = torch.empty(max(rdf2v_skipgram_pairs_workspace_size(w), 1), dtype=torch.uint8, device=dev)
+    if count is None:
+        count = torch.empty(1, dtype=torch.int64, device=dev)
+
+    def call(out, cap):
+        st = _native().rdf2v_skipgram_pairs(_ptr(tokens), _ptr(lens), w, width, window, _ptr(out), cap,
+                                          _ptr(count), _ptr(workspace), workspace.numel(), _ptr(status),
+                                          _stream(dev, stream))
+        _check(st, "rdf2v_skipgram_pairs")
+
+    if pairs is not None:
+        call(pairs, int(pairs.shape[0]))
+        return pairs, count
+    call(None, 0)
+    n = int(count.item())
+    out = torch.empty((n, 2), dtype=torch.int32, device=dev)
+    call(out, n)
+    return out
+
+
 def check_device_status(status: torch.Tensor, where: str = "device") -> None:
     """Raise if a device status word (zeroed before the calls) has any bit set."""
     v = int(status.item())
     if v != 0:
         bits = [n for b, n in [(RDF2V_STATUS_ID_OUT_OF_RANGE, "ID_OUT_OF_RANGE"),
-                               (RDF2V_STATUS_BAD_CSR, "BAD_CSR")] if v & b]
+                               (RDF2V_STATUS_BAD_CSR, "BAD_CSR"), (RDF2V_STATUS_BAD_LENGTH, "BAD_LENGTH"),
+                               (RDF2V_STATUS_CAPACITY, "CAPACITY")] if v & b]
         raise Rdf2vError(RDF2V_ERR_ID_OUT_OF_RANGE, f"{where}: status bits {'|'.join(bits) or v}")

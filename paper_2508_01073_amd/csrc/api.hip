@@ -125,6 +125,31 @@ RDF2V_API rdf2v_status rdf2v_random_walks(const rdf2v_csr *csr, const int32_t *s
   return rdf2v::launch_random_walks(a, static_cast<hipStream_t>(stream));
 }
 
+RDF2V_API size_t rdf2v_skipgram_pairs_workspace_size(int64_t num_walks) {
+  if (num_walks < 0) return 0;
+  return rdf2v::skipgram_workspace_bytes(num_walks);
+}
+
+RDF2V_API rdf2v_status rdf2v_skipgram_pairs(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                            int32_t row_width, int32_t window, int32_t *pairs_out,
+                                            int64_t pair_capacity, int64_t *pair_count_out,
+                                            void *workspace, size_t workspace_bytes,
+                                            int32_t *status_dev, void *stream) {
+  if (num_walks < 0 || window < 0 || pair_capacity < 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (row_width < 1 || row_width > 2 * RDF2V_MAX_DEPTH + 1) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (pair_count_out == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (num_walks > 0 && (tokens == nullptr || len == nullptr)) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (pair_capacity > 0 && pairs_out == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if ((reinterpret_cast<uintptr_t>(pairs_out) & 7) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (num_walks > INT64_MAX / (2 * int64_t(row_width))) return RDF2V_ERR_TOO_LARGE;
+  const size_t need = rdf2v::skipgram_workspace_bytes(num_walks);
+  if (workspace == nullptr || workspace_bytes < need) return RDF2V_ERR_WORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return RDF2V_ERR_WORKSPACE;
+  return rdf2v::launch_skipgram_pairs(tokens, len, num_walks, row_width, window, pairs_out,
+                                      pair_capacity, pair_count_out, workspace, status_dev,
+                                      static_cast<hipStream_t>(stream));
+}
+
 RDF2V_API const char *rdf2v_status_string(rdf2v_status status) {
   switch (status) {
     case RDF2V_OK: return "RDF2V_OK";

@@ -27,28 +27,28 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 __device__ __forceinline__ uint64_t lanes_below(int lane) { return (uint64_t(1) << lane) - 1; }
 
-// Exclusive scan of one int per thread over a block of NT threads (NT a
-// multiple of 64, at most 1024). `scratch` holds NT/64 ints of LDS. Returns the
-// thread's exclusive prefix; `total` receives the block-wide sum. Contains two
-// block barriers, so every thread of the block must call it.
-template <int NT>
-__device__ __forceinline__ int block_exclusive_scan(int x, int *scratch, int &total) {
+// Exclusive scan of one value per thread over a block of NT threads (NT a
+// multiple of 64, at most 1024). `scratch` holds NT/64 values of LDS. Returns
+// the thread's exclusive prefix; `total` receives the block-wide sum. Contains
+// two block barriers, so every thread of the block must call it.
+template <int NT, typename T = int>
+__device__ __forceinline__ T block_exclusive_scan(T x, T *scratch, T &total) {
   constexpr int kWaves = NT / kWave;
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  int v = x;
+  T v = x;
 #pragma unroll
   for (int off = 1; off < kWave; off <<= 1) {
-    const int y = __shfl_up(v, off, kWave);
+    const T y = __shfl_up(v, off, kWave);
     if (lane >= off) v += y;
   }
   if (lane == kWave - 1) scratch[wave] = v;
   __syncthreads();
-  int before = 0, sum = 0;
+  T before = 0, sum = 0;
 #pragma unroll
   for (int i = 0; i < kWaves; ++i) {
-    const int s = scratch[i];
-    before += (i < wave) ? s : 0;
+    const T s = scratch[i];
+    before += (i < wave) ? s : T(0);
     sum += s;
   }
   __syncthreads();
@@ -56,11 +56,11 @@ __device__ __forceinline__ int block_exclusive_scan(int x, int *scratch, int &to
   return before + v - x;
 }
 
-// Sum of one int per thread over the block (same contract as above).
-template <int NT>
-__device__ __forceinline__ int block_sum(int x, int *scratch) {
-  int total;
-  (void)block_exclusive_scan<NT>(x, scratch, total);
+// Sum of one value per thread over the block (same contract as above).
+template <int NT, typename T = int>
+__device__ __forceinline__ T block_sum(T x, T *scratch) {
+  T total;
+  (void)block_exclusive_scan<NT, T>(x, scratch, total);
   return total;
 }
 

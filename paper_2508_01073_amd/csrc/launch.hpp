@@ -56,4 +56,10 @@ rdf2v_status launch_walk_edges(const int32_t *row_ptr, const int32_t *edges, int
                                int32_t num_entities, int32_t *walk_edges_out, int32_t *status_dev,
                                hipStream_t stream);
 
+size_t skipgram_workspace_bytes(int64_t num_walks);
+rdf2v_status launch_skipgram_pairs(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                   int32_t width, int32_t window, int32_t *pairs_out, int64_t capacity,
+                                   int64_t *count_out, void *workspace, int32_t *status_dev,
+                                   hipStream_t stream);
+
 }  // namespace rdf2v

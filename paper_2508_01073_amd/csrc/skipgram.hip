@@ -1,0 +1,243 @@
+// Skip-gram training pairs from walk rows on gfx950.
+//
+// gpuRDF2vec turns the walk corpus into center-context pairs for SkipGram
+// (Sec. 3.2) after dropping the -1 padding (Sec. 3.1). For walk r with
+// L = len[r] valid tokens t_0 .. t_{L-1}, every center i and every context j
+// with 1 <= |i - j| <= window, 0 <= j < L, give the pair (t_i, t_j), ordered
+// by walk, then i, then j.
+//
+// The number of pairs of a walk is a closed form of L and the window, so the
+// output offsets of all walks are one exclusive scan (int64: a corpus easily
+// exceeds 2^31 pairs) and the emit kernel needs no atomics: one thread per
+// (walk, center) computes where its pairs start, again in closed form, and
+// places them. Pure integer streaming work, bound by HBM writes.
+
+#include <algorithm>
+
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace rdf2v {
+namespace {
+
+typedef int32_t v2i32 __attribute__((ext_vector_type(2)));
+typedef int32_t v4i32 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kItems = 16;
+constexpr int kTile = kThreads * kItems;  // walks per scan block
+
+// Pairs of a walk with L valid tokens: 2 * sum_{d=1}^{m} (L - d), m = min(window, L - 1).
+__device__ __forceinline__ int64_t walk_pairs(int64_t L, int64_t window) {
+  const int64_t m = min(window, L - 1);
+  return m <= 0 ? 0 : 2 * (m * L - m * (m + 1) / 2);
+}
+
+// sum_{k=0}^{n-1} min(k, window)
+__device__ __forceinline__ int64_t capped_prefix(int64_t n, int64_t window) {
+  if (n <= 0) return 0;
+  if (n <= window + 1) return n * (n - 1) / 2;
+  return window * (window + 1) / 2 + (n - 1 - window) * window;
+}
+
+// Valid length of walk r, clamped to the row; out-of-range lengths raise a flag.
+__device__ __forceinline__ int32_t clamped_len(const int32_t *len, int64_t r, int32_t width, int &bad) {
+  const int32_t L = len[r];
+  if (L < 0 || L > width) {
+    bad = 1;
+    return L < 0 ? 0 : width;
+  }
+  return L;
+}
+
+__global__ __launch_bounds__(kThreads) void pair_count_reduce_kernel(const int32_t *__restrict__ len,
+                                                                     int64_t n, int32_t width,
+                                                                     int32_t window,
+                                                                     int64_t *__restrict__ partials,
+                                                                     int32_t *status) {
+  __shared__ int64_t scratch[kThreads / kWave];
+  const int64_t base = int64_t(blockIdx.x) * kTile;
+  int64_t s = 0;
+  int bad = 0;
+#pragma unroll 4
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t r = base + int64_t(i) * kThreads + threadIdx.x;
+    if (r < n) s += walk_pairs(clamped_len(len, r, width, bad), window);
+  }
+  const int64_t total = block_sum<kThreads, int64_t>(s, scratch);
+  if (threadIdx.x == 0) partials[blockIdx.x] = total;
+  if (bad && status != nullptr) atomicOr(status, RDF2V_STATUS_BAD_LENGTH);
+}
+
+// One block: exclusive scan of the block sums in place; the total goes to *total_out.
+__global__ __launch_bounds__(kThreads) void pair_partials_kernel(int64_t *partials, int64_t nb,
+                                                                 int64_t *total_out) {
+  __shared__ int64_t scratch[kThreads / kWave];
+  int64_t carry = 0;
+  for (int64_t base = 0; base < nb; base += kThreads) {
+    const int64_t idx = base + threadIdx.x;
+    const int64_t x = idx < nb ? partials[idx] : 0;
+    int64_t tot;
+    const int64_t ex = block_exclusive_scan<kThreads, int64_t>(x, scratch, tot);
+    if (idx < nb) partials[idx] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) {
+    partials[nb] = carry;
+    *total_out = carry;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void pair_offsets_kernel(const int32_t *__restrict__ len, int64_t n,
+                                                                int32_t width, int32_t window,
+                                                                const int64_t *__restrict__ partials,
+                                                                int64_t *__restrict__ offsets) {
+  __shared__ int64_t scratch[kThreads / kWave];
+  const int64_t base = int64_t(blockIdx.x) * kTile;
+  int64_t carry = partials[blockIdx.x];
+  int bad = 0;
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t r = base + int64_t(i) * kThreads + threadIdx.x;
+    const int64_t x = r < n ? walk_pairs(clamped_len(len, r, width, bad), window) : 0;
+    int64_t tot;
+    const int64_t ex = block_exclusive_scan<kThreads, int64_t>(x, scratch, tot);
+    if (r < n) offsets[r] = carry + ex;
+    carry += tot;
+  }
+}
+
+// One thread per (walk, center); walks_per_block = kThreads / width walks per
+// block, whose pairs form one contiguous output range. When that range fits in
+// LDS (kStagePairs), the threads place their pairs there and the block streams
+// the range out with consecutive, non-temporal 8-byte stores; otherwise each
+// thread writes its pairs directly.
+constexpr int kStagePairs = 4096;
+
+template <bool kStage>
+__global__ __launch_bounds__(kThreads) void pair_emit_kernel(const int32_t *__restrict__ tokens,
+                                                             const int32_t *__restrict__ len, int64_t n,
+                                                             int32_t width, int32_t window,
+                                                             const int64_t *__restrict__ offsets,
+                                                             int2 *__restrict__ pairs, int64_t capacity,
+                                                             int32_t *status) {
+  __shared__ int2 stage[kStage ? kStagePairs : 1];
+  const int walks_per_block = kThreads / width;
+  const int t = threadIdx.x;
+  const int64_t r0 = int64_t(blockIdx.x) * walks_per_block;
+  const int64_t r_end = min(n, r0 + walks_per_block);
+  const int64_t r = r0 + t / width;
+  const int64_t i = t % width;
+  const bool active = t < walks_per_block * width && r < n;
+  int bad = 0;
+  const int64_t w = window;
+  const int64_t block_first = offsets[r0];
+  int64_t first = 0, L = 0;
+  if (active) {
+    L = clamped_len(len, r, width, bad);
+    first = offsets[r] + capped_prefix(i, w) + capped_prefix(L, w) - capped_prefix(L - i, w);
+  }
+  bool full = false;
+  if (active && i < L) {
+    const int32_t *row = tokens + r * width;
+    const int32_t center = row[i];
+    const int64_t j0 = max(int64_t(0), i - w), j1 = min(L - 1, i + w);
+    int64_t k = first;
+    for (int64_t j = j0; j <= j1; ++j) {
+      if (j == i) continue;
+      const int2 pr = make_int2(center, row[j]);
+      if (kStage) {
+        stage[k - block_first] = pr;
+      } else if (k < capacity) {
+        __builtin_nontemporal_store(v2i32{pr.x, pr.y}, reinterpret_cast<v2i32 *>(pairs + k));
+      } else {
+        full = true;
+      }
+      ++k;
+    }
+  }
+  if (kStage) {
+    __syncthreads();
+    // The block's pairs end where the next block's begin: the offset of walk
+    // r_end, or the pair count of the last walk added to its offset.
+    __shared__ int64_t block_end;
+    if (t == 0) {
+      int b2 = 0;
+      const int64_t last = r_end - 1;
+      const int64_t Ll = clamped_len(len, last, width, b2);
+      block_end = offsets[last] + walk_pairs(Ll, w);
+    }
+    __syncthreads();
+    const int64_t cnt = block_end - block_first;
+    if (block_end > capacity) full = true;
+    const int64_t lim = min(cnt, capacity - block_first);  // pairs of this block that fit
+    // One leading pair if the range does not start 16-byte aligned, then two
+    // pairs per 16-byte store, then a possible trailing pair.
+    const int64_t head = (reinterpret_cast<uintptr_t>(pairs + block_first) & 15) ? 1 : 0;
+    if (t == 0 && head && lim > 0)
+      __builtin_nontemporal_store(v2i32{stage[0].x, stage[0].y}, reinterpret_cast<v2i32 *>(pairs + block_first));
+    const int64_t body = lim > head ? (lim - head) >> 1 : 0;
+    v4i32 *dst = reinterpret_cast<v4i32 *>(pairs + block_first + head);
+    for (int64_t q = t; q < body; q += kThreads) {
+      const int2 a = stage[head + 2 * q], b = stage[head + 2 * q + 1];
+      __builtin_nontemporal_store(v4i32{a.x, a.y, b.x, b.y}, dst + q);
+    }
+    const int64_t tail = head + 2 * body;
+    if (t == 0 && tail < lim)
+      __builtin_nontemporal_store(v2i32{stage[tail].x, stage[tail].y},
+                                  reinterpret_cast<v2i32 *>(pairs + block_first + tail));
+  }
+  if ((full || bad) && status != nullptr)
+    atomicOr(status, (full ? RDF2V_STATUS_CAPACITY : 0) | (bad ? RDF2V_STATUS_BAD_LENGTH : 0));
+}
+
+// Most pairs one walk of this width can give.
+inline int64_t max_walk_pairs(int64_t width, int64_t window) {
+  const int64_t m = std::min(window, width - 1);
+  return m <= 0 ? 0 : 2 * (m * width - m * (m + 1) / 2);
+}
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+size_t skipgram_workspace_bytes(int64_t num_walks) {
+  const int64_t nb = ceil_div(num_walks, kTile);
+  return align_up(size_t(num_walks) * 8, 256) + align_up(size_t(nb + 1) * 8, 256);
+}
+
+rdf2v_status launch_skipgram_pairs(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                   int32_t width, int32_t window, int32_t *pairs_out, int64_t capacity,
+                                   int64_t *count_out, void *workspace, int32_t *status_dev,
+                                   hipStream_t stream) {
+  char *ws = static_cast<char *>(workspace);
+  int64_t *offsets = reinterpret_cast<int64_t *>(ws);
+  int64_t *partials = reinterpret_cast<int64_t *>(ws + align_up(size_t(num_walks) * 8, 256));
+  const int64_t nb = ceil_div(num_walks, kTile);
+  if (nb > 0) {
+    pair_count_reduce_kernel<<<dim3(unsigned(nb)), dim3(kThreads), 0, stream>>>(len, num_walks, width, window,
+                                                                               partials, status_dev);
+    RDF2V_LAUNCH_CHECK();
+  }
+  pair_partials_kernel<<<dim3(1), dim3(kThreads), 0, stream>>>(partials, nb, count_out);
+  RDF2V_LAUNCH_CHECK();
+  if (nb == 0) return RDF2V_OK;
+  pair_offsets_kernel<<<dim3(unsigned(nb)), dim3(kThreads), 0, stream>>>(len, num_walks, width, window,
+                                                                        partials, offsets);
+  RDF2V_LAUNCH_CHECK();
+  if (capacity > 0) {
+    const int walks_per_block = kThreads / width;
+    const int64_t blocks = ceil_div(num_walks, walks_per_block);
+    if (blocks >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
+    int2 *out = reinterpret_cast<int2 *>(pairs_out);
+    if (max_walk_pairs(width, window) * walks_per_block <= kStagePairs)
+      pair_emit_kernel<true><<<dim3(unsigned(blocks)), dim3(kThreads), 0, stream>>>(
+          tokens, len, num_walks, width, window, offsets, out, capacity, status_dev);
+    else
+      pair_emit_kernel<false><<<dim3(unsigned(blocks)), dim3(kThreads), 0, stream>>>(
+          tokens, len, num_walks, width, window, offsets, out, capacity, status_dev);
+    RDF2V_LAUNCH_CHECK();
+  }
+  return RDF2V_OK;
+}
+
+}  // namespace rdf2v

@@ -31,7 +31,8 @@ def lib():
 def test_header_declares_the_calls():
     names = _declared_functions()
     for n in ["rdf2v_build_csr", "rdf2v_build_csr_workspace_size", "rdf2v_random_walks", "rdf2v_build_walk_edges",
-              "rdf2v_nonsink_starts", "rdf2v_nonsink_starts_workspace_size", "rdf2v_status_string"]:
+              "rdf2v_nonsink_starts", "rdf2v_nonsink_starts_workspace_size", "rdf2v_status_string",
+              "rdf2v_skipgram_pairs", "rdf2v_skipgram_pairs_workspace_size"]:
         assert n in names
 
 
@@ -148,6 +149,36 @@ def test_walk_edges_argument_validation(lib):
     # walks reading walk records need them 16-byte aligned
     c = pkg._CsrStruct(10, 3, 20, FAKE, FAKE8, ctypes.c_void_p((1 << 40) + 8))
     assert _walk(lib, c) == E_INV
+
+
+def test_skipgram_argument_validation(lib):
+    so, pkg = lib
+    f = so.rdf2v_skipgram_pairs
+    need = pkg.rdf2v_skipgram_pairs_workspace_size(100)
+    WS = ctypes.c_void_p(1 << 41)
+    E_INV = pkg.RDF2V_ERR_INVALID_ARGUMENT
+    ok_args = dict(tokens=FAKE, len=FAKE, n=100, width=9, window=5, pairs=FAKE8, cap=10, count=FAKE,
+                   ws=WS, wsb=need)
+
+    def call(**kw):
+        a = dict(ok_args, **kw)
+        return f(a["tokens"], a["len"], a["n"], a["width"], a["window"], a["pairs"], a["cap"], a["count"],
+                 a["ws"], a["wsb"], None, None)
+
+    assert call(n=-1) == E_INV
+    assert call(window=-1) == E_INV
+    assert call(cap=-1) == E_INV
+    assert call(width=0) == E_INV
+    assert call(width=130) == E_INV
+    assert call(count=None) == E_INV
+    assert call(tokens=None) == E_INV
+    assert call(len=None) == E_INV
+    assert call(pairs=None) == E_INV
+    assert call(pairs=ctypes.c_void_p((1 << 40) + 4)) == E_INV
+    assert call(ws=None) == pkg.RDF2V_ERR_WORKSPACE
+    assert call(wsb=need - 1) == pkg.RDF2V_ERR_WORKSPACE
+    assert pkg.rdf2v_skipgram_pairs_workspace_size(0) > 0
+    assert pkg.rdf2v_skipgram_pairs_workspace_size(10**6) >= 8 * 10**6
 
 
 def test_nonsink_argument_validation(lib):
