@@ -67,6 +67,12 @@ def _load():
                                            ctypes.c_int32, ctypes.c_uint64, ctypes.c_int64,
                                            ctypes.c_int64, i32p, i32p]
     lib.rdf2v_ref_random_walks.restype = ctypes.c_int
+    lib.rdf2v_ref_project_walks.argtypes = [i32p, i32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                            i32p, i32p]
+    lib.rdf2v_ref_project_walks.restype = ctypes.c_int
+    lib.rdf2v_ref_unique_walks.argtypes = [i32p, i32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                           i32p, i32p]
+    lib.rdf2v_ref_unique_walks.restype = ctypes.c_int64
     lib.rdf2v_ref_skipgram_pairs.argtypes = [i32p, i32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                              i32p, ctypes.c_int64]
     lib.rdf2v_ref_skipgram_pairs.restype = ctypes.c_int64
@@ -176,3 +182,37 @@ def skipgram_pairs(tokens, lens, window: int) -> np.ndarray:
     pairs = np.empty((n, 2), dtype=np.int32)
     lib.rdf2v_ref_skipgram_pairs(_ptr(tok), _ptr(ln), w, width, window, _ptr(pairs), n)
     return pairs
+
+
+ENTITY_WALKS = 1
+PROPERTY_WALKS = 2
+
+
+def project_walks(tokens, lens, depth: int, kind: int):
+    """Entity walks (kind 1: entity tokens) or property walks (kind 2: start entity, then the
+    predicate tokens) of triple-based walk rows; rows of depth + 1 tokens padded with -1."""
+    lib = _load()
+    tok = _i32(tokens)
+    ln = _i32(lens)
+    n = ln.shape[0]
+    out = np.empty((n, depth + 1), dtype=np.int32)
+    out_len = np.empty(n, dtype=np.int32)
+    st = lib.rdf2v_ref_project_walks(_ptr(tok), _ptr(ln), n, depth, kind, _ptr(out), _ptr(out_len))
+    if st != OK:
+        raise OracleError(st, "rdf2v_ref_project_walks")
+    return out, out_len
+
+
+def unique_walks(tokens, lens, group_size: int):
+    """Duplicate-free walks: within each group of group_size consecutive rows (the walks of one
+    start entity), the first occurrence of every distinct walk, in order -> (rows, lens)."""
+    lib = _load()
+    tok = _i32(tokens)
+    ln = _i32(lens)
+    n, width = tok.shape
+    out = np.empty((n, width), dtype=np.int32)
+    out_len = np.empty(n, dtype=np.int32)
+    k = lib.rdf2v_ref_unique_walks(_ptr(tok), _ptr(ln), n, group_size, width, _ptr(out), _ptr(out_len))
+    if k < 0:
+        raise OracleError(int(-k), "rdf2v_ref_unique_walks")
+    return out[:k].copy(), out_len[:k].copy()

@@ -218,6 +218,64 @@ int rdf2v_ref_random_walks(const int32_t *row_ptr, const int32_t *edges, int32_t
   return REF_OK;
 }
 
+// Entity walks and property walks (Tab. 1 lists both among the walk kinds;
+// the paper does not define them further). They are read here as projections
+// of the triple-based walk on the same random stream:
+//   kind 1, entity walk:   e_0, e_1, ..., e_h   (the entity tokens),
+//   kind 2, property walk: e_0, V+p_0, ..., V+p_{h-1}   (the start entity and
+//                          the predicate tokens),
+// each padded with -1 to depth + 1 tokens; out_len = h + 1. Input rows are
+// triple-based walks of 2*depth+1 tokens with len = 2h+1.
+int rdf2v_ref_project_walks(const int32_t *tokens, const int32_t *len, int64_t num_walks, int32_t depth,
+                            int32_t kind, int32_t *out, int32_t *out_len) {
+  if (num_walks < 0 || depth < 0 || depth > kMaxDepth || (kind != 1 && kind != 2))
+    return REF_ERR_INVALID_ARGUMENT;
+  const int64_t in_width = 2 * int64_t(depth) + 1, out_width = int64_t(depth) + 1;
+  for (int64_t r = 0; r < num_walks; ++r) {
+    const int32_t *row = tokens + r * in_width;
+    int32_t *dst = out + r * out_width;
+    const int64_t L = len[r];
+    if (L < 1 || L > in_width || L % 2 == 0) return REF_ERR_INVALID_ARGUMENT;
+    const int64_t hops = (L - 1) / 2;
+    dst[0] = row[0];
+    for (int64_t h = 0; h < hops; ++h) dst[1 + h] = (kind == 1) ? row[2 * h + 2] : row[2 * h + 1];
+    for (int64_t j = hops + 1; j < out_width; ++j) dst[j] = -1;
+    out_len[r] = int32_t(hops + 1);
+  }
+  return REF_OK;
+}
+
+// Duplicate-free walks (Tab. 1: "random walk duplicate free"): among the walks
+// of one start entity, keep only the first occurrence (in walk-id order) of
+// each distinct walk. Rows come in groups of group_size consecutive rows (the
+// walks_per_node walks of one start; the last group may be shorter); two rows
+// are the same walk when their lengths and their first len tokens agree.
+// Kept rows are copied, in order, to out / out_len; returns how many.
+int64_t rdf2v_ref_unique_walks(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                               int32_t group_size, int32_t row_width, int32_t *out, int32_t *out_len) {
+  if (num_walks < 0 || group_size < 1 || row_width < 1) return -REF_ERR_INVALID_ARGUMENT;
+  int64_t kept = 0;
+  for (int64_t r = 0; r < num_walks; ++r) {
+    const int64_t g0 = r / group_size * group_size;
+    const int32_t *row = tokens + r * row_width;
+    bool seen = false;
+    for (int64_t q = g0; q < r && !seen; ++q) {
+      if (len[q] != len[r]) continue;
+      const int32_t *other = tokens + q * row_width;
+      bool same = true;
+      for (int32_t j = 0; j < len[r] && same; ++j) same = other[j] == row[j];
+      seen = same;
+    }
+    if (seen) continue;
+    if (out != nullptr) {
+      for (int32_t j = 0; j < row_width; ++j) out[kept * row_width + j] = row[j];
+      out_len[kept] = len[r];
+    }
+    ++kept;
+  }
+  return kept;
+}
+
 // Skip-gram training pairs (Sec. 3.2: the data module turns the walk corpus
 // into center-context pairs; Sec. 3.1: padding is dropped first). For walk r
 // with L = len[r] valid tokens t_0 .. t_{L-1}, every center position i and

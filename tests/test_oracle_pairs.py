@@ -84,3 +84,71 @@ def test_capacity_truncates_but_counts_all():
     out = np.full((3, 2), -7, np.int32)
     n = lib.rdf2v_ref_skipgram_pairs(oracle._ptr(tok), oracle._ptr(ln), 1, 3, 1, oracle._ptr(out), 2)
     assert n == 4 and out[:2].tolist() == [[1, 2], [2, 1]] and out[2].tolist() == [-7, -7]
+
+
+# ----------------------------------------------------------------------------
+# Entity walks and property walks (projections of the triple-based walk)
+# ----------------------------------------------------------------------------
+
+def test_projection_hand_worked():
+    V = 100
+    # walk 7 -p3-> 8 -p1-> 9 (2 hops of depth 3), and a sink start 5
+    tok = np.array([[7, V + 3, 8, V + 1, 9, -1, -1], [5, -1, -1, -1, -1, -1, -1]], np.int32)
+    ln = np.array([5, 1], np.int32)
+    ent, el = oracle.project_walks(tok, ln, 3, oracle.ENTITY_WALKS)
+    assert ent.tolist() == [[7, 8, 9, -1], [5, -1, -1, -1]] and el.tolist() == [3, 1]
+    prop, pl = oracle.project_walks(tok, ln, 3, oracle.PROPERTY_WALKS)
+    assert prop.tolist() == [[7, V + 3, V + 1, -1], [5, -1, -1, -1]] and pl.tolist() == [3, 1]
+
+
+def test_projection_matches_slicing_on_real_walks():
+    w = synth.WORKLOADS["tiny_uniform"]
+    s, p, o = synth.triples(w)
+    V = w.num_entities
+    rp, ed = oracle.build_csr(s, p, o, V, w.num_predicates)
+    st = oracle.nonsink_starts(rp, V)
+    d = 6
+    tok, ln = oracle.random_walks(rp, ed, V, w.num_predicates, st, 3, d, 42)
+    ent, el = oracle.project_walks(tok, ln, d, oracle.ENTITY_WALKS)
+    prop, pl = oracle.project_walks(tok, ln, d, oracle.PROPERTY_WALKS)
+    assert np.array_equal(el, (ln + 1) // 2) and np.array_equal(pl, (ln + 1) // 2)
+    for r in range(tok.shape[0]):
+        L = int(ln[r])
+        assert ent[r, :el[r]].tolist() == tok[r, 0:L:2].tolist()          # even positions
+        assert prop[r, :pl[r]].tolist() == [int(tok[r, 0])] + tok[r, 1:L:2].tolist()
+        assert np.all(ent[r, el[r]:] == -1) and np.all(prop[r, pl[r]:] == -1)
+        assert np.all(ent[r, :el[r]] < V) and np.all(prop[r, 1:pl[r]] >= V)
+
+
+# ----------------------------------------------------------------------------
+# Duplicate-free walks
+# ----------------------------------------------------------------------------
+
+def test_unique_walks_hand_worked():
+    tok = np.array([[1, 5, 2], [1, 5, 2], [1, 6, 3], [1, -1, -1], [1, 5, 2],   # group of start 1
+                    [4, 5, 2], [4, -1, -1], [4, -1, 9]], np.int32)            # group of start 4
+    ln = np.array([3, 3, 3, 1, 3, 3, 1, 1], np.int32)
+    rows, lens = oracle.unique_walks(tok, ln, 5)
+    # rows 1 and 4 repeat row 0; row 7 equals row 6 on its valid prefix (padding ignored)
+    assert rows.tolist() == [[1, 5, 2], [1, 6, 3], [1, -1, -1], [4, 5, 2], [4, -1, -1]]
+    assert lens.tolist() == [3, 3, 1, 3, 1]
+
+
+def test_unique_walks_match_set_construction():
+    # tiny graph with few distinct walks: many duplicates per start
+    rp, ed = oracle.build_csr(np.array([0, 0, 1, 1, 2], np.int32), np.array([0, 1, 0, 0, 1], np.int32),
+                              np.array([1, 2, 2, 0, 0], np.int32), 3, 2)
+    starts = np.array([0, 1, 2, 0], np.int32)
+    wpn = 40
+    tok, ln = oracle.random_walks(rp, ed, 3, 2, starts, wpn, 4, 42)
+    rows, lens = oracle.unique_walks(tok, ln, wpn)
+    expect = []
+    for g in range(len(starts)):
+        seen = set()
+        for r in range(g * wpn, (g + 1) * wpn):
+            key = tuple(tok[r, :ln[r]].tolist())
+            if key not in seen:
+                seen.add(key)
+                expect.append(r)
+    assert np.array_equal(rows, tok[expect]) and np.array_equal(lens, ln[expect])
+    assert len(expect) < tok.shape[0]
