@@ -41,19 +41,20 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def useful_bytes(lens, depth: int, num_start: int) -> tuple[int, int, int]:
+def useful_bytes(lens, depth: int, num_start: int, kind: int = 0) -> tuple[int, int, int]:
     """(useful bytes, hops, valid tokens) of one walk launch.
 
     Gathered: 16 B per hop (the row_ptr pair and one (predicate, object) record),
     8 B more for a walk that stops at a sink (the row_ptr pair that shows it), and
-    4 B per start id. Written: the padded token row (4 * (2*depth+1) B) and the
-    length (4 B) of every walk."""
+    4 B per start id. Written: the padded token row (4 * width B: width = 2*depth+1
+    for triple rows, depth+1 for entity or property rows) and the length (4 B)."""
     import torch
-    width = 2 * depth + 1
+    width = 2 * depth + 1 if kind == 0 else depth + 1
+    per_hop = 2 if kind == 0 else 1
     ln = lens.to(torch.int64)
     tokens = int(ln.sum().item())
     walks = int(ln.numel())
-    hops = (tokens - walks) // 2
+    hops = (tokens - walks) // per_hop
     early = int((lens < width).sum().item())
     gathered = 16 * hops + 8 * early + 4 * num_start
     written = walks * (4 * width + 4)
@@ -149,6 +150,37 @@ def time_pairs(rd, torch, tokens, lens, n_walks, batch_cap, width, window, pair_
     }
 
 
+def time_unique(rd, torch, tokens, lens, n_walks, batch_cap, wpn, stream, ev):
+    """Time rdf2v_unique_walks over the walk rows left in the output buffer (groups of
+    walks_per_node rows). Algorithmic bytes: rows and lengths read once, kept rows written."""
+    dev = tokens.device
+    rows = min(n_walks, batch_cap) // wpn * wpn
+    tok, ln = tokens[:rows], lens[:rows]
+    out_t = torch.empty_like(tok)
+    out_l = torch.empty_like(ln)
+    count = torch.empty(1, dtype=torch.int64, device=dev)
+    ws = torch.empty(rd.rdf2v_unique_walks_workspace_size(rows), dtype=torch.uint8, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    call = lambda: rd.rdf2v_unique_walks(tok, ln, wpn, tokens_out=out_t, lens_out=out_l, count=count,
+                                         workspace=ws, status=status, stream=stream, sync=False)
+    call()
+    torch.cuda.synchronize()
+    rd.check_device_status(status, "unique walks")
+    kept = int(count.item())
+    e0, e1 = ev(), ev()
+    e0.record(stream)
+    for _ in range(3):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 3
+    width = tok.shape[1]
+    useful = rows * (4 * width + 4) + kept * (4 * width + 4)
+    return {"walks": rows, "kept": kept, "ms": ms, "walks_per_s": rows / (ms * 1e-3),
+            "achieved_GBps": useful / (ms * 1e-3) / 1e9,
+            "frac_of_hbm_peak": useful / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -157,6 +189,10 @@ def main() -> int:
     ap.add_argument("--workload", default="powerlaw_20m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--tokens", choices=["triples", "entities", "properties"], default="triples",
+                    help="walk rows: entity/predicate triples (default), entity walks or property walks")
+    ap.add_argument("--unique-walks", action="store_true",
+                    help="also time duplicate-free filtering of the corpus (per start entity)")
     ap.add_argument("--pairs-window", type=int, default=0,
                     help="also time skip-gram pair generation over the corpus with this window "
                          "(0: off)")
@@ -199,7 +235,9 @@ def main() -> int:
     count = torch.empty(1, dtype=torch.int64, device=dev)
     status = torch.zeros(1, dtype=torch.int32, device=dev)
     max_walks = V * wpn
-    width = 2 * d + 1
+    kind = {"triples": rd.RDF2V_TOKENS_TRIPLES, "entities": rd.RDF2V_TOKENS_ENTITIES,
+            "properties": rd.RDF2V_TOKENS_PROPERTIES}[args.tokens]
+    width = 2 * d + 1 if kind == rd.RDF2V_TOKENS_TRIPLES else d + 1
     # Walks are produced in batches of w.batch_walks into one reused buffer when the
     # workload asks for it (the 500M-triple share); otherwise in one launch.
     batch_cap = min(max_walks, w.batch_walks) if w.batch_walks else max_walks
@@ -239,12 +277,12 @@ def main() -> int:
         launches = 0
         for b0 in range(0, n_walks, batch_cap):
             c = min(batch_cap, n_walks - b0)
-            rd.rdf2v_random_walks(csr, st[:n_start], wpn, d, 42, b0, c, tokens=tokens[:c],
-                                  lens=lens[:c], status=status, stream=stream)
+            rd.rdf2v_random_walks_tokens(csr, st[:n_start], wpn, d, 42, b0, c, kind, tokens=tokens[:c],
+                                         lens=lens[:c], status=status, stream=stream)
             launches += 1
             if measure is not None:
                 starts_read = (b0 + c + wpn - 1) // wpn - b0 // wpn
-                measure.append(useful_bytes(lens[:c], d, starts_read))
+                measure.append(useful_bytes(lens[:c], d, starts_read, kind))
         e3.record(stream)
         record.append((e0, e1, e2, e3, n_start, launches))
 
@@ -318,6 +356,9 @@ def main() -> int:
         "walk_kernel_hops_per_s": hops / (walk_ms * 1e-3),
         "padded_token_slots_per_s": n_walks * width / (walk_ms * 1e-3),
     }
+    out["config"]["tokens"] = args.tokens
+    if args.unique_walks:
+        out["unique_walks"] = time_unique(rd, torch, tokens, lens, n_walks, batch_cap, wpn, stream, ev)
     if args.pairs_window > 0:
         out["skipgram_pairs"] = time_pairs(rd, torch, tokens, lens, n_walks, batch_cap, width,
                                            args.pairs_window, args.pairs_batch_walks, stream, ev)

@@ -215,6 +215,51 @@ rdf2v_status rdf2v_skipgram_pairs(const int32_t *tokens, const int32_t *len, int
                                   int64_t pair_capacity, int64_t *pair_count_out, void *workspace,
                                   size_t workspace_bytes, int32_t *status_dev, void *stream);
 
+/* Which tokens a walk row holds (Tab. 1 lists entity walks and property walks
+ * beside triple-based random walks). All three follow the same walk, drawn
+ * from the same random stream, so an entity or property walk is exactly the
+ * projection of the triple-based walk with the same walk id. */
+typedef enum rdf2v_walk_tokens {
+  RDF2V_TOKENS_TRIPLES = 0,   /* e_0, V+p_0, e_1, ..., e_h: 2*depth+1 tokens per row */
+  RDF2V_TOKENS_ENTITIES = 1,  /* e_0, e_1, ..., e_h: depth+1 tokens per row */
+  RDF2V_TOKENS_PROPERTIES = 2 /* e_0, V+p_0, ..., V+p_{h-1}: depth+1 tokens per row */
+} rdf2v_walk_tokens;
+
+/*
+ * rdf2v_random_walks with a choice of tokens: identical arguments plus
+ * token_kind; tokens_out holds walk_count rows of 2*depth+1 (TRIPLES) or
+ * depth+1 (ENTITIES, PROPERTIES) tokens, padded with -1, and len_out the
+ * valid tokens per row (2*hops+1 or hops+1).
+ */
+rdf2v_status rdf2v_random_walks_tokens(const rdf2v_csr *csr, const int32_t *start_nodes,
+                                       int64_t num_start, int32_t walks_per_node, int32_t depth,
+                                       uint64_t seed, int64_t walk_begin, int64_t walk_count,
+                                       int32_t token_kind, int32_t *tokens_out, int32_t *len_out,
+                                       int32_t *status_dev, void *stream);
+
+/* Bytes of device workspace rdf2v_unique_walks needs. Pure host function. */
+size_t rdf2v_unique_walks_workspace_size(int64_t num_walks);
+
+/*
+ * Duplicate-free walks (Tab. 1: "random walk duplicate free"): rows come in
+ * groups of group_size consecutive rows (the walks of one start entity, as
+ * rdf2v_random_walks writes them for walks_per_node = group_size; the last
+ * group may be shorter). Within each group only the first occurrence, in row
+ * order, of each distinct walk is kept; two rows are the same walk when their
+ * lengths and their first len tokens agree. Kept rows are written, in order,
+ * to tokens_out / len_out, and their number to *count_out (device int64).
+ *
+ *   tokens, len      [num_walks][row_width] and [num_walks] int32 (device).
+ *   tokens_out, len_out  room for num_walks rows (device); must not alias the
+ *                    inputs.
+ *   workspace        rdf2v_unique_walks_workspace_size(num_walks) bytes of
+ *                    device scratch, 256-byte aligned.
+ */
+rdf2v_status rdf2v_unique_walks(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                int32_t group_size, int32_t row_width, int32_t *tokens_out,
+                                int32_t *len_out, int64_t *count_out, void *workspace,
+                                size_t workspace_bytes, int32_t *status_dev, void *stream);
+
 /* Static, human-readable name of a status code. */
 const char *rdf2v_status_string(rdf2v_status status);
 

@@ -23,9 +23,11 @@ import torch
 
 __all__ = [
     "Csr", "Rdf2vError", "RDF2V_MAX_DEPTH", "RDF2V_STATUS_ID_OUT_OF_RANGE", "RDF2V_STATUS_BAD_CSR",
+    "RDF2V_TOKENS_TRIPLES", "RDF2V_TOKENS_ENTITIES", "RDF2V_TOKENS_PROPERTIES",
     "rdf2v_build_csr_workspace_size", "rdf2v_build_csr", "rdf2v_build_walk_edges",
     "rdf2v_nonsink_starts_workspace_size",
-    "rdf2v_nonsink_starts", "rdf2v_random_walks", "rdf2v_skipgram_pairs_workspace_size",
+    "rdf2v_nonsink_starts", "rdf2v_random_walks", "rdf2v_random_walks_tokens",
+    "rdf2v_unique_walks_workspace_size", "rdf2v_unique_walks", "rdf2v_skipgram_pairs_workspace_size",
     "rdf2v_skipgram_pairs", "rdf2v_status_string", "check_device_status",
     "library_path",
 ]
@@ -43,6 +45,9 @@ RDF2V_STATUS_BAD_CSR = 0x2
 RDF2V_STATUS_BAD_LENGTH = 0x4
 RDF2V_STATUS_CAPACITY = 0x8
 RDF2V_MAX_DEPTH = 64
+RDF2V_TOKENS_TRIPLES = 0
+RDF2V_TOKENS_ENTITIES = 1
+RDF2V_TOKENS_PROPERTIES = 2
 
 _lib = None
 
@@ -79,6 +84,12 @@ def _native():
     lib.rdf2v_nonsink_starts.restype = ctypes.c_int
     lib.rdf2v_random_walks.argtypes = [csr_p, vp, i64, i32, i32, u64, i64, i64, vp, vp, vp, vp]
     lib.rdf2v_random_walks.restype = ctypes.c_int
+    lib.rdf2v_random_walks_tokens.argtypes = [csr_p, vp, i64, i32, i32, u64, i64, i64, i32, vp, vp, vp, vp]
+    lib.rdf2v_random_walks_tokens.restype = ctypes.c_int
+    lib.rdf2v_unique_walks_workspace_size.argtypes = [i64]
+    lib.rdf2v_unique_walks_workspace_size.restype = sz
+    lib.rdf2v_unique_walks.argtypes = [vp, vp, i64, i32, i32, vp, vp, vp, vp, sz, vp, vp]
+    lib.rdf2v_unique_walks.restype = ctypes.c_int
     lib.rdf2v_skipgram_pairs_workspace_size.argtypes = [i64]
     lib.rdf2v_skipgram_pairs_workspace_size.restype = sz
     lib.rdf2v_skipgram_pairs.argtypes = [vp, vp, i64, i32, i32, vp, i64, vp, vp, sz, vp, vp]
@@ -224,12 +235,29 @@ def rdf2v_random_walks(csr: Csr, start_nodes: torch.Tensor, walks_per_node: int,
                        status: torch.Tensor | None = None, stream=None):
     """Walks [walk_begin, walk_begin + walk_count) -> (tokens int32 [walk_count, 2*depth+1],
     lens int32 [walk_count]). Walk w starts at start_nodes[w // walks_per_node]."""
+    return _walks(csr, start_nodes, walks_per_node, depth, seed, walk_begin, walk_count,
+                  RDF2V_TOKENS_TRIPLES, tokens, lens, status, stream, "rdf2v_random_walks")
+
+
+def rdf2v_random_walks_tokens(csr: Csr, start_nodes: torch.Tensor, walks_per_node: int, depth: int,
+                              seed: int, walk_begin: int = 0, walk_count: int | None = None,
+                              token_kind: int = RDF2V_TOKENS_TRIPLES, *,
+                              tokens: torch.Tensor | None = None, lens: torch.Tensor | None = None,
+                              status: torch.Tensor | None = None, stream=None):
+    """Like rdf2v_random_walks with a choice of tokens: RDF2V_TOKENS_TRIPLES (2*depth+1 per row),
+    RDF2V_TOKENS_ENTITIES or RDF2V_TOKENS_PROPERTIES (depth+1 per row)."""
+    return _walks(csr, start_nodes, walks_per_node, depth, seed, walk_begin, walk_count, token_kind,
+                  tokens, lens, status, stream, "rdf2v_random_walks_tokens")
+
+
+def _walks(csr, start_nodes, walks_per_node, depth, seed, walk_begin, walk_count, token_kind,
+           tokens, lens, status, stream, where):
     _dev_i32(start_nodes, "start_nodes")
     dev = start_nodes.device
     num_walks = start_nodes.shape[0] * walks_per_node
     if walk_count is None:
         walk_count = num_walks - walk_begin
-    width = 2 * depth + 1
+    width = 2 * depth + 1 if token_kind == RDF2V_TOKENS_TRIPLES else depth + 1
     if tokens is None:
         tokens = torch.empty((max(walk_count, 0), max(width, 1)), dtype=torch.int32, device=dev)
     if lens is None:
@@ -237,12 +265,45 @@ def rdf2v_random_walks(csr: Csr, start_nodes: torch.Tensor, walks_per_node: int,
     if walk_count > 0 and (tokens.numel() < walk_count * width or lens.numel() < walk_count):
         raise ValueError("output buffers too small for walk_count rows")
     c = csr._c()
-    st = _native().rdf2v_random_walks(ctypes.byref(c), _ptr(start_nodes), start_nodes.shape[0],
-                                 walks_per_node, depth, ctypes.c_uint64(seed & (2**64 - 1)),
-                                 walk_begin, walk_count, _ptr(tokens), _ptr(lens), _ptr(status),
-                                 _stream(dev, stream))
-    _check(st, "rdf2v_random_walks")
+    st = _native().rdf2v_random_walks_tokens(ctypes.byref(c), _ptr(start_nodes), start_nodes.shape[0],
+                                             walks_per_node, depth, ctypes.c_uint64(seed & (2**64 - 1)),
+                                             walk_begin, walk_count, token_kind, _ptr(tokens), _ptr(lens),
+                                             _ptr(status), _stream(dev, stream))
+    _check(st, where)
     return tokens, lens
+
+
+def rdf2v_unique_walks_workspace_size(num_walks: int) -> int:
+    return int(_native().rdf2v_unique_walks_workspace_size(num_walks))
+
+
+def rdf2v_unique_walks(tokens: torch.Tensor, lens: torch.Tensor, group_size: int, *,
+                       tokens_out: torch.Tensor | None = None, lens_out: torch.Tensor | None = None,
+                       count: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                       status: torch.Tensor | None = None, stream=None, sync: bool = True):
+    """Duplicate-free walks: within each group of group_size consecutive rows keep the first
+    occurrence of each distinct walk. With sync=True returns the kept (tokens, lens) (one
+    device-to-host read of the count); else (tokens_out, lens_out, count_device_int64)."""
+    _dev_i32(tokens, "tokens"); _dev_i32(lens, "lens")
+    dev = tokens.device
+    n = int(lens.shape[0])
+    width = int(tokens.shape[1]) if tokens.dim() == 2 else 1
+    if tokens_out is None:
+        tokens_out = torch.empty((n, width), dtype=torch.int32, device=dev)
+    if lens_out is None:
+        lens_out = torch.empty(n, dtype=torch.int32, device=dev)
+    if count is None:
+        count = torch.empty(1, dtype=torch.int64, device=dev)
+    if workspace is None:
+        workspace = torch.empty(max(rdf2v_unique_walks_workspace_size(n), 1), dtype=torch.uint8, device=dev)
+    st = _native().rdf2v_unique_walks(_ptr(tokens), _ptr(lens), n, group_size, width, _ptr(tokens_out),
+                                      _ptr(lens_out), _ptr(count), _ptr(workspace), workspace.numel(),
+                                      _ptr(status), _stream(dev, stream))
+    _check(st, "rdf2v_unique_walks")
+    if not sync:
+        return tokens_out, lens_out, count
+    k = int(count.item())
+    return tokens_out[:k], lens_out[:k]
 
 
 def rdf2v_skipgram_pairs_workspace_size(num_walks: int) -> int:

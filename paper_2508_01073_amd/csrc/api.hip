@@ -83,6 +83,19 @@ RDF2V_API rdf2v_status rdf2v_random_walks(const rdf2v_csr *csr, const int32_t *s
                                           uint64_t seed, int64_t walk_begin, int64_t walk_count,
                                           int32_t *tokens_out, int32_t *len_out,
                                           int32_t *status_dev, void *stream) {
+  return rdf2v_random_walks_tokens(csr, start_nodes, num_start, walks_per_node, depth, seed, walk_begin,
+                                   walk_count, RDF2V_TOKENS_TRIPLES, tokens_out, len_out, status_dev,
+                                   stream);
+}
+
+RDF2V_API rdf2v_status rdf2v_random_walks_tokens(const rdf2v_csr *csr, const int32_t *start_nodes,
+                                                 int64_t num_start, int32_t walks_per_node, int32_t depth,
+                                                 uint64_t seed, int64_t walk_begin, int64_t walk_count,
+                                                 int32_t token_kind, int32_t *tokens_out, int32_t *len_out,
+                                                 int32_t *status_dev, void *stream) {
+  if (token_kind != RDF2V_TOKENS_TRIPLES && token_kind != RDF2V_TOKENS_ENTITIES &&
+      token_kind != RDF2V_TOKENS_PROPERTIES)
+    return RDF2V_ERR_INVALID_ARGUMENT;
   if (csr == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
   if (csr->num_entities < 0 || csr->num_predicates < 0 || csr->num_edges < 0)
     return RDF2V_ERR_INVALID_ARGUMENT;
@@ -120,6 +133,7 @@ RDF2V_API rdf2v_status rdf2v_random_walks(const rdf2v_csr *csr, const int32_t *s
   a.num_predicates = csr->num_predicates;
   a.walks_per_node = walks_per_node;
   a.depth = depth;
+  a.token_kind = token_kind;
   a.key_lo = uint32_t(seed);
   a.key_hi = uint32_t(seed >> 32);
   return rdf2v::launch_random_walks(a, static_cast<hipStream_t>(stream));
@@ -148,6 +162,27 @@ RDF2V_API rdf2v_status rdf2v_skipgram_pairs(const int32_t *tokens, const int32_t
   return rdf2v::launch_skipgram_pairs(tokens, len, num_walks, row_width, window, pairs_out,
                                       pair_capacity, pair_count_out, workspace, status_dev,
                                       static_cast<hipStream_t>(stream));
+}
+
+RDF2V_API size_t rdf2v_unique_walks_workspace_size(int64_t num_walks) {
+  if (num_walks < 0) return 0;
+  return rdf2v::unique_walks_workspace_bytes(num_walks);
+}
+
+RDF2V_API rdf2v_status rdf2v_unique_walks(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                          int32_t group_size, int32_t row_width, int32_t *tokens_out,
+                                          int32_t *len_out, int64_t *count_out, void *workspace,
+                                          size_t workspace_bytes, int32_t *status_dev, void *stream) {
+  if (num_walks < 0 || group_size < 1 || row_width < 1) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (count_out == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (num_walks > 0 && (tokens == nullptr || len == nullptr || tokens_out == nullptr || len_out == nullptr))
+    return RDF2V_ERR_INVALID_ARGUMENT;
+  if (num_walks > (int64_t(1) << 31) * 255 || num_walks > INT64_MAX / row_width) return RDF2V_ERR_TOO_LARGE;
+  const size_t need = rdf2v::unique_walks_workspace_bytes(num_walks);
+  if (workspace == nullptr || workspace_bytes < need) return RDF2V_ERR_WORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return RDF2V_ERR_WORKSPACE;
+  return rdf2v::launch_unique_walks(tokens, len, num_walks, group_size, row_width, tokens_out, len_out,
+                                    count_out, workspace, status_dev, static_cast<hipStream_t>(stream));
 }
 
 RDF2V_API const char *rdf2v_status_string(rdf2v_status status) {

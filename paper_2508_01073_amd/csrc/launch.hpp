@@ -47,6 +47,7 @@ struct WalkArgs {
   int32_t num_predicates;
   int32_t walks_per_node;
   int32_t depth;
+  int32_t token_kind;  // rdf2v_walk_tokens
   uint32_t key_lo;
   uint32_t key_hi;
 };
@@ -61,5 +62,11 @@ rdf2v_status launch_skipgram_pairs(const int32_t *tokens, const int32_t *len, in
                                    int32_t width, int32_t window, int32_t *pairs_out, int64_t capacity,
                                    int64_t *count_out, void *workspace, int32_t *status_dev,
                                    hipStream_t stream);
+
+size_t unique_walks_workspace_bytes(int64_t num_walks);
+rdf2v_status launch_unique_walks(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                 int32_t group, int32_t width, int32_t *tokens_out, int32_t *len_out,
+                                 int64_t *count_out, void *workspace, int32_t *status_dev,
+                                 hipStream_t stream);
 
 }  // namespace rdf2v

@@ -67,10 +67,13 @@ __device__ __forceinline__ Words4 philox_block(uint32_t hop_block, uint64_t walk
 // kFused: read (predicate, object, row lo, row hi) records, so each hop is one
 // 16-byte gather; otherwise read (predicate, object) and then the row bounds
 // of the object (two dependent gathers per hop).
-template <int kBlock, bool kFused>
+// kKind selects the tokens a hop appends: RDF2V_TOKENS_TRIPLES (predicate and
+// entity), RDF2V_TOKENS_ENTITIES (entity) or RDF2V_TOKENS_PROPERTIES
+// (predicate). The walk itself, and its random stream, is the same for all.
+template <int kBlock, bool kFused, int kKind>
 __global__ __launch_bounds__(kBlock) void random_walk_kernel(const WalkArgs a) {
   extern __shared__ __align__(16) int32_t tile[];
-  const int width = 2 * a.depth + 1;
+  const int width = kKind == RDF2V_TOKENS_TRIPLES ? 2 * a.depth + 1 : a.depth + 1;
   const int64_t row0 = int64_t(blockIdx.x) * kBlock;
   const int nrows = int(min(int64_t(kBlock), a.walk_count - row0));
   const int t = threadIdx.x;
@@ -134,9 +137,14 @@ __global__ __launch_bounds__(kBlock) void random_walk_kernel(const WalkArgs a) {
           alive = false;
           break;
         }
-        row[len] = int32_t(V) + p;
-        row[len + 1] = x;
-        len += 2;
+        if (kKind == RDF2V_TOKENS_TRIPLES) {
+          row[len] = int32_t(V) + p;
+          row[len + 1] = x;
+          len += 2;
+        } else {
+          row[len] = kKind == RDF2V_TOKENS_ENTITIES ? x : int32_t(V) + p;
+          len += 1;
+        }
         e = x;
       }
     }
@@ -204,16 +212,26 @@ __global__ __launch_bounds__(kWalkEdgeThreads) void walk_edges_kernel(
   if (bad && status != nullptr) atomicOr(status, RDF2V_STATUS_ID_OUT_OF_RANGE);
 }
 
+template <int kBlock, int kKind>
+void launch_kind(const WalkArgs &a, int64_t blocks, size_t lds, hipStream_t stream) {
+  if (a.walk_edges != nullptr)
+    random_walk_kernel<kBlock, true, kKind><<<dim3(unsigned(blocks)), dim3(kBlock), lds, stream>>>(a);
+  else
+    random_walk_kernel<kBlock, false, kKind><<<dim3(unsigned(blocks)), dim3(kBlock), lds, stream>>>(a);
+}
+
 template <int kBlock>
 rdf2v_status launch_walk_kernel(const WalkArgs &a, hipStream_t stream) {
-  const int width = 2 * a.depth + 1;
+  const int width = a.token_kind == RDF2V_TOKENS_TRIPLES ? 2 * a.depth + 1 : a.depth + 1;
   const int64_t blocks = (a.walk_count + kBlock - 1) / kBlock;
   if (blocks >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
   const size_t lds = size_t(kBlock) * width * 4;
-  if (a.walk_edges != nullptr)
-    random_walk_kernel<kBlock, true><<<dim3(unsigned(blocks)), dim3(kBlock), lds, stream>>>(a);
-  else
-    random_walk_kernel<kBlock, false><<<dim3(unsigned(blocks)), dim3(kBlock), lds, stream>>>(a);
+  switch (a.token_kind) {
+    case RDF2V_TOKENS_TRIPLES: launch_kind<kBlock, RDF2V_TOKENS_TRIPLES>(a, blocks, lds, stream); break;
+    case RDF2V_TOKENS_ENTITIES: launch_kind<kBlock, RDF2V_TOKENS_ENTITIES>(a, blocks, lds, stream); break;
+    case RDF2V_TOKENS_PROPERTIES: launch_kind<kBlock, RDF2V_TOKENS_PROPERTIES>(a, blocks, lds, stream); break;
+    default: return RDF2V_ERR_INVALID_ARGUMENT;
+  }
   RDF2V_LAUNCH_CHECK();
   return RDF2V_OK;
 }

@@ -32,7 +32,8 @@ def test_header_declares_the_calls():
     names = _declared_functions()
     for n in ["rdf2v_build_csr", "rdf2v_build_csr_workspace_size", "rdf2v_random_walks", "rdf2v_build_walk_edges",
               "rdf2v_nonsink_starts", "rdf2v_nonsink_starts_workspace_size", "rdf2v_status_string",
-              "rdf2v_skipgram_pairs", "rdf2v_skipgram_pairs_workspace_size"]:
+              "rdf2v_skipgram_pairs", "rdf2v_skipgram_pairs_workspace_size", "rdf2v_random_walks_tokens",
+              "rdf2v_unique_walks", "rdf2v_unique_walks_workspace_size"]:
         assert n in names
 
 
@@ -179,6 +180,28 @@ def test_skipgram_argument_validation(lib):
     assert call(wsb=need - 1) == pkg.RDF2V_ERR_WORKSPACE
     assert pkg.rdf2v_skipgram_pairs_workspace_size(0) > 0
     assert pkg.rdf2v_skipgram_pairs_workspace_size(10**6) >= 8 * 10**6
+
+
+def test_token_kind_and_unique_validation(lib):
+    so, pkg = lib
+    c = _csr(pkg)
+    f = so.rdf2v_random_walks_tokens
+    for kind in (-1, 3, 7):
+        assert f(ctypes.byref(c), FAKE, 5, 2, 4, 42, 0, 10, kind, FAKE, FAKE, None, None) == \
+            pkg.RDF2V_ERR_INVALID_ARGUMENT
+    # a valid kind still goes through the walk argument checks
+    assert f(ctypes.byref(c), FAKE, 5, 2, 65, 42, 0, 10, 1, FAKE, FAKE, None, None) == pkg.RDF2V_ERR_INVALID_ARGUMENT
+    u = so.rdf2v_unique_walks
+    need = pkg.rdf2v_unique_walks_workspace_size(100)
+    WS = ctypes.c_void_p(1 << 41)
+    E_INV = pkg.RDF2V_ERR_INVALID_ARGUMENT
+    assert u(FAKE, FAKE, -1, 5, 9, FAKE, FAKE, FAKE, WS, need, None, None) == E_INV
+    assert u(FAKE, FAKE, 100, 0, 9, FAKE, FAKE, FAKE, WS, need, None, None) == E_INV
+    assert u(FAKE, FAKE, 100, 5, 0, FAKE, FAKE, FAKE, WS, need, None, None) == E_INV
+    assert u(FAKE, FAKE, 100, 5, 9, FAKE, FAKE, None, WS, need, None, None) == E_INV
+    assert u(FAKE, FAKE, 100, 5, 9, None, FAKE, FAKE, WS, need, None, None) == E_INV
+    assert u(FAKE, FAKE, 100, 5, 9, FAKE, FAKE, FAKE, None, need, None, None) == pkg.RDF2V_ERR_WORKSPACE
+    assert u(FAKE, FAKE, 100, 5, 9, FAKE, FAKE, FAKE, WS, need - 1, None, None) == pkg.RDF2V_ERR_WORKSPACE
 
 
 def test_nonsink_argument_validation(lib):
