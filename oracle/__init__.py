@@ -73,6 +73,9 @@ def _load():
     lib.rdf2v_ref_unique_walks.argtypes = [i32p, i32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                            i32p, i32p]
     lib.rdf2v_ref_unique_walks.restype = ctypes.c_int64
+    lib.rdf2v_ref_bfs_walks.argtypes = [i32p, i32p, ctypes.c_int32, ctypes.c_int32, i32p, ctypes.c_int64,
+                                        ctypes.c_int32, ctypes.c_int32, i32p, i32p, i32p]
+    lib.rdf2v_ref_bfs_walks.restype = ctypes.c_int64
     lib.rdf2v_ref_skipgram_pairs.argtypes = [i32p, i32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                              i32p, ctypes.c_int64]
     lib.rdf2v_ref_skipgram_pairs.restype = ctypes.c_int64
@@ -216,3 +219,24 @@ def unique_walks(tokens, lens, group_size: int):
     if k < 0:
         raise OracleError(int(-k), "rdf2v_ref_unique_walks")
     return out[:k].copy(), out_len[:k].copy()
+
+
+def bfs_walks(row_ptr, edges, num_entities: int, num_predicates: int, roots, depth: int, max_walks: int):
+    """BFS walks: per root, the root-to-leaf paths of its depth-limited queue-order BFS tree
+    (first max_walks leaves in the order reached). Returns (tokens[R, max_walks, 2*depth+1],
+    len[R, max_walks], counts[R], number of roots with more leaves than max_walks); rows past
+    counts[r] are not written (filled with -1 / 0 here)."""
+    lib = _load()
+    rp = _i32(row_ptr)
+    ed = _i32(edges).reshape(-1)
+    rt = _i32(roots)
+    R = rt.shape[0]
+    width = 2 * depth + 1
+    tokens = np.full((R, max_walks, width), -1, dtype=np.int32)
+    lens = np.zeros((R, max_walks), dtype=np.int32)
+    counts = np.zeros(R, dtype=np.int32)
+    k = lib.rdf2v_ref_bfs_walks(_ptr(rp), _ptr(ed), num_entities, num_predicates, _ptr(rt), R, depth,
+                                max_walks, _ptr(tokens), _ptr(lens), _ptr(counts))
+    if k < 0:
+        raise OracleError(int(-k), "rdf2v_ref_bfs_walks")
+    return tokens, lens, counts, int(k)

@@ -276,6 +276,71 @@ int64_t rdf2v_ref_unique_walks(const int32_t *tokens, const int32_t *len, int64_
   return kept;
 }
 
+// BFS walks (Sec. 3.1): a breadth-first search from each root gives every
+// reached entity one predecessor, the first entity that reaches it, and every
+// path from a leaf of that tree back to the root becomes one walk, so each
+// entity appears in at most one walk per root. Read here as a queue-order BFS
+// limited to `depth` hops: entities of one level are expanded in the order in
+// which they were reached, each through its out-edge records in CSR order, and
+// an entity not reached before gets the current entity and record as its
+// parent. A tree entity with no child (including every entity at the depth
+// limit) is a leaf; leaves are taken in the order they were reached, and the
+// first max_walks of them give the walks root, V+p_1, v_1, ..., leaf (rows of
+// 2*depth+1 tokens padded with -1). counts[r] = number of walks written for
+// root r; the return value is the number of roots whose leaves did not fit.
+int64_t rdf2v_ref_bfs_walks(const int32_t *row_ptr, const int32_t *edges, int32_t num_entities,
+                            int32_t num_predicates, const int32_t *roots, int64_t num_roots, int32_t depth,
+                            int32_t max_walks, int32_t *tokens, int32_t *len, int32_t *counts) {
+  if (num_entities < 0 || num_roots < 0 || depth < 0 || depth > kMaxDepth || max_walks < 1)
+    return -REF_ERR_INVALID_ARGUMENT;
+  const int64_t width = 2 * int64_t(depth) + 1;
+  std::vector<int32_t> seen_root(size_t(num_entities), -1);  // root index that reached the entity
+  struct Node { int32_t entity, parent, pred, level; bool has_child; };
+  int64_t truncated = 0;
+  for (int64_t r = 0; r < num_roots; ++r) {
+    const int32_t root = roots[r];
+    if (root < 0 || root >= num_entities) return -REF_ERR_ID_OUT_OF_RANGE;
+    std::vector<Node> tree;
+    tree.push_back({root, -1, -1, 0, false});
+    seen_root[size_t(root)] = int32_t(r);
+    size_t level_begin = 0, level_end = 1;
+    for (int32_t level = 0; level < depth && level_begin < level_end; ++level) {
+      for (size_t i = level_begin; i < level_end; ++i) {
+        const int32_t u = tree[i].entity;
+        for (int64_t k = row_ptr[u]; k < row_ptr[u + 1]; ++k) {
+          const int32_t p = edges[2 * k], x = edges[2 * k + 1];
+          if (seen_root[size_t(x)] == int32_t(r)) continue;
+          seen_root[size_t(x)] = int32_t(r);
+          tree[i].has_child = true;
+          tree.push_back({x, int32_t(i), p, level + 1, false});
+        }
+      }
+      level_begin = level_end;
+      level_end = tree.size();
+    }
+    int32_t written = 0;
+    for (size_t i = 0; i < tree.size(); ++i) {
+      if (tree[i].has_child) continue;
+      if (written == max_walks) { ++truncated; break; }
+      int32_t *row = tokens + (r * int64_t(max_walks) + written) * width;
+      const int32_t h = tree[i].level;
+      int32_t node = int32_t(i);
+      for (int32_t step = h; step >= 1; --step) {  // fill from the leaf back to the root
+        row[2 * step] = tree[size_t(node)].entity;
+        row[2 * step - 1] = num_entities + tree[size_t(node)].pred;
+        node = tree[size_t(node)].parent;
+      }
+      row[0] = root;
+      for (int64_t j = 2 * int64_t(h) + 1; j < width; ++j) row[j] = -1;
+      len[r * int64_t(max_walks) + written] = 2 * h + 1;
+      ++written;
+    }
+    counts[r] = written;
+  }
+  (void)num_predicates;
+  return truncated;
+}
+
 // Skip-gram training pairs (Sec. 3.2: the data module turns the walk corpus
 // into center-context pairs; Sec. 3.1: padding is dropped first). For walk r
 // with L = len[r] valid tokens t_0 .. t_{L-1}, every center position i and
