@@ -150,6 +150,39 @@ def time_pairs(rd, torch, tokens, lens, n_walks, batch_cap, width, window, pair_
     }
 
 
+def csr_for_bfs(rd, row_ptr, edges, V, P):
+    return rd.Csr(row_ptr, edges, V, P)
+
+
+def time_bfs(rd, torch, csr, roots, depth, max_walks, stream, ev):
+    """Time rdf2v_bfs_walks from every start entity. Bytes: the walk rows written (the
+    traversal's own reads depend on the trees and are not counted)."""
+    dev = roots.device
+    R = int(roots.shape[0])
+    width = 2 * depth + 1
+    tok = torch.empty((R, max_walks, width), dtype=torch.int32, device=dev)
+    ln = torch.empty((R, max_walks), dtype=torch.int32, device=dev)
+    cnt = torch.empty(R, dtype=torch.int32, device=dev)
+    ws = torch.empty(rd.rdf2v_bfs_walks_workspace_size(csr.num_entities, R), dtype=torch.uint8, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    call = lambda: rd.rdf2v_bfs_walks(csr, roots, depth, max_walks, tokens=tok, lens=ln, counts=cnt,
+                                      workspace=ws, status=status, stream=stream)
+    call()
+    torch.cuda.synchronize()
+    walks = int(cnt.to(torch.int64).sum().item())
+    truncated = bool(int(status.item()) & rd.RDF2V_STATUS_CAPACITY)
+    e0, e1 = ev(), ev()
+    e0.record(stream)
+    for _ in range(3):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 3
+    return {"depth": depth, "roots": R, "max_walks_per_root": max_walks, "walks": walks,
+            "some_roots_truncated": truncated, "ms": ms, "roots_per_s": R / (ms * 1e-3),
+            "walks_per_s": walks / (ms * 1e-3)}
+
+
 def time_unique(rd, torch, tokens, lens, n_walks, batch_cap, wpn, stream, ev):
     """Time rdf2v_unique_walks over the walk rows left in the output buffer (groups of
     walks_per_node rows). Algorithmic bytes: rows and lengths read once, kept rows written."""
@@ -193,6 +226,9 @@ def main() -> int:
                     help="walk rows: entity/predicate triples (default), entity walks or property walks")
     ap.add_argument("--unique-walks", action="store_true",
                     help="also time duplicate-free filtering of the corpus (per start entity)")
+    ap.add_argument("--bfs-depth", type=int, default=-1,
+                    help="also time BFS walks from every start entity with this depth (-1: off)")
+    ap.add_argument("--bfs-max-walks", type=int, default=256)
     ap.add_argument("--pairs-window", type=int, default=0,
                     help="also time skip-gram pair generation over the corpus with this window "
                          "(0: off)")
@@ -359,6 +395,9 @@ def main() -> int:
     out["config"]["tokens"] = args.tokens
     if args.unique_walks:
         out["unique_walks"] = time_unique(rd, torch, tokens, lens, n_walks, batch_cap, wpn, stream, ev)
+    if args.bfs_depth >= 0:
+        out["bfs_walks"] = time_bfs(rd, torch, csr_for_bfs(rd, row_ptr, edges, V, P), starts[:n_start],
+                                    args.bfs_depth, args.bfs_max_walks, stream, ev)
     if args.pairs_window > 0:
         out["skipgram_pairs"] = time_pairs(rd, torch, tokens, lens, n_walks, batch_cap, width,
                                            args.pairs_window, args.pairs_batch_walks, stream, ev)

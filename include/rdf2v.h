@@ -260,6 +260,37 @@ rdf2v_status rdf2v_unique_walks(const int32_t *tokens, const int32_t *len, int64
                                 int32_t *len_out, int64_t *count_out, void *workspace,
                                 size_t workspace_bytes, int32_t *status_dev, void *stream);
 
+/* Bytes of device workspace rdf2v_bfs_walks needs. Pure host function. */
+size_t rdf2v_bfs_walks_workspace_size(int32_t num_entities, int64_t num_roots);
+
+/*
+ * BFS walks (gpuRDF2vec Sec. 3.1: a BFS from each root gives every reached
+ * entity one predecessor, the first entity to reach it, and each leaf-to-root
+ * path of that tree is one walk, so an entity appears at most once per root).
+ *
+ * The tree is that of a queue-order BFS limited to `depth` hops: the entities
+ * of one level are expanded in the order they were reached, each through its
+ * out-edge records in CSR order, and an entity not yet in the tree gets the
+ * current entity and record as its parent. Tree entities without a child
+ * (including every entity at the depth limit) are leaves; in the order they
+ * were reached, the first max_walks of them give the walks
+ * root, V+p_1, v_1, ..., leaf.
+ *
+ *   csr          CSR view (row_ptr and edges are read).
+ *   roots        [num_roots] int32 entity ids (device).
+ *   tokens_out   [num_roots][max_walks][2 * depth + 1] int32 (device): the
+ *                first counts_out[r] rows of root r are written (padded with
+ *                -1); the rest are left untouched.
+ *   len_out      [num_roots][max_walks] int32, written like tokens_out.
+ *   counts_out   [num_roots] int32: walks written per root. A root with more
+ *                leaves than max_walks raises RDF2V_STATUS_CAPACITY.
+ *   workspace    rdf2v_bfs_walks_workspace_size(V, num_roots) bytes (at most
+ *                about 4 GiB), 256-byte aligned.
+ */
+rdf2v_status rdf2v_bfs_walks(const rdf2v_csr *csr, const int32_t *roots, int64_t num_roots, int32_t depth,
+                             int32_t max_walks, int32_t *tokens_out, int32_t *len_out, int32_t *counts_out,
+                             void *workspace, size_t workspace_bytes, int32_t *status_dev, void *stream);
+
 /* Static, human-readable name of a status code. */
 const char *rdf2v_status_string(rdf2v_status status);
 

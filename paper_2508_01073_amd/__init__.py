@@ -27,7 +27,8 @@ __all__ = [
     "rdf2v_build_csr_workspace_size", "rdf2v_build_csr", "rdf2v_build_walk_edges",
     "rdf2v_nonsink_starts_workspace_size",
     "rdf2v_nonsink_starts", "rdf2v_random_walks", "rdf2v_random_walks_tokens",
-    "rdf2v_unique_walks_workspace_size", "rdf2v_unique_walks", "rdf2v_skipgram_pairs_workspace_size",
+    "rdf2v_unique_walks_workspace_size", "rdf2v_unique_walks", "rdf2v_bfs_walks_workspace_size",
+    "rdf2v_bfs_walks", "rdf2v_skipgram_pairs_workspace_size",
     "rdf2v_skipgram_pairs", "rdf2v_status_string", "check_device_status",
     "library_path",
 ]
@@ -90,6 +91,10 @@ def _native():
     lib.rdf2v_unique_walks_workspace_size.restype = sz
     lib.rdf2v_unique_walks.argtypes = [vp, vp, i64, i32, i32, vp, vp, vp, vp, sz, vp, vp]
     lib.rdf2v_unique_walks.restype = ctypes.c_int
+    lib.rdf2v_bfs_walks_workspace_size.argtypes = [i32, i64]
+    lib.rdf2v_bfs_walks_workspace_size.restype = sz
+    lib.rdf2v_bfs_walks.argtypes = [csr_p, vp, i64, i32, i32, vp, vp, vp, vp, sz, vp, vp]
+    lib.rdf2v_bfs_walks.restype = ctypes.c_int
     lib.rdf2v_skipgram_pairs_workspace_size.argtypes = [i64]
     lib.rdf2v_skipgram_pairs_workspace_size.restype = sz
     lib.rdf2v_skipgram_pairs.argtypes = [vp, vp, i64, i32, i32, vp, i64, vp, vp, sz, vp, vp]
@@ -304,6 +309,37 @@ def rdf2v_unique_walks(tokens: torch.Tensor, lens: torch.Tensor, group_size: int
         return tokens_out, lens_out, count
     k = int(count.item())
     return tokens_out[:k], lens_out[:k]
+
+
+def rdf2v_bfs_walks_workspace_size(num_entities: int, num_roots: int) -> int:
+    return int(_native().rdf2v_bfs_walks_workspace_size(num_entities, num_roots))
+
+
+def rdf2v_bfs_walks(csr: Csr, roots: torch.Tensor, depth: int, max_walks: int, *,
+                    tokens: torch.Tensor | None = None, lens: torch.Tensor | None = None,
+                    counts: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                    status: torch.Tensor | None = None, stream=None):
+    """BFS walks per root -> (tokens [R, max_walks, 2*depth+1], lens [R, max_walks], counts [R]);
+    rows past counts[r] are left as allocated (filled with -1 / 0 when allocated here)."""
+    _dev_i32(roots, "roots")
+    dev = roots.device
+    R = int(roots.shape[0])
+    width = 2 * depth + 1
+    if tokens is None:
+        tokens = torch.full((R, max_walks, width), -1, dtype=torch.int32, device=dev)
+    if lens is None:
+        lens = torch.zeros((R, max_walks), dtype=torch.int32, device=dev)
+    if counts is None:
+        counts = torch.empty(R, dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = torch.empty(max(rdf2v_bfs_walks_workspace_size(csr.num_entities, R), 1),
+                                dtype=torch.uint8, device=dev)
+    c = csr._c()
+    st = _native().rdf2v_bfs_walks(ctypes.byref(c), _ptr(roots), R, depth, max_walks, _ptr(tokens), _ptr(lens),
+                                   _ptr(counts), _ptr(workspace), workspace.numel(), _ptr(status),
+                                   _stream(dev, stream))
+    _check(st, "rdf2v_bfs_walks")
+    return tokens, lens, counts
 
 
 def rdf2v_skipgram_pairs_workspace_size(num_walks: int) -> int:

@@ -185,6 +185,37 @@ RDF2V_API rdf2v_status rdf2v_unique_walks(const int32_t *tokens, const int32_t *
                                     count_out, workspace, status_dev, static_cast<hipStream_t>(stream));
 }
 
+RDF2V_API size_t rdf2v_bfs_walks_workspace_size(int32_t num_entities, int64_t num_roots) {
+  if (num_entities < 0 || num_roots < 0) return 0;
+  return rdf2v::bfs_walks_workspace_bytes(num_entities, num_roots);
+}
+
+RDF2V_API rdf2v_status rdf2v_bfs_walks(const rdf2v_csr *csr, const int32_t *roots, int64_t num_roots,
+                                       int32_t depth, int32_t max_walks, int32_t *tokens_out,
+                                       int32_t *len_out, int32_t *counts_out, void *workspace,
+                                       size_t workspace_bytes, int32_t *status_dev, void *stream) {
+  if (csr == nullptr || csr->row_ptr == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (csr->num_entities < 0 || csr->num_predicates < 0 || csr->num_edges < 0)
+    return RDF2V_ERR_INVALID_ARGUMENT;
+  if (num_roots < 0 || depth < 0 || depth > RDF2V_MAX_DEPTH || max_walks < 1) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (csr->num_edges >= kInt32Limit || id_space_too_large(csr->num_entities, csr->num_predicates))
+    return RDF2V_ERR_TOO_LARGE;
+  // the per-level stamps of one workgroup must not run out
+  if (num_roots > 0 && (num_roots + 1) * int64_t(depth + 1) >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
+  if (num_roots > INT64_MAX / max_walks / (2 * int64_t(depth) + 1)) return RDF2V_ERR_TOO_LARGE;
+  if (num_roots == 0) return RDF2V_OK;
+  if (roots == nullptr || tokens_out == nullptr || len_out == nullptr || counts_out == nullptr)
+    return RDF2V_ERR_INVALID_ARGUMENT;
+  if (csr->num_edges > 0 && csr->edges == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if ((reinterpret_cast<uintptr_t>(csr->edges) & 7) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  const size_t need = rdf2v::bfs_walks_workspace_bytes(csr->num_entities, num_roots);
+  if (workspace == nullptr || workspace_bytes < need) return RDF2V_ERR_WORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return RDF2V_ERR_WORKSPACE;
+  return rdf2v::launch_bfs_walks(csr->row_ptr, csr->edges, csr->num_edges, csr->num_entities,
+                                 csr->num_predicates, roots, num_roots, depth, max_walks, tokens_out, len_out,
+                                 counts_out, workspace, status_dev, static_cast<hipStream_t>(stream));
+}
+
 RDF2V_API const char *rdf2v_status_string(rdf2v_status status) {
   switch (status) {
     case RDF2V_OK: return "RDF2V_OK";

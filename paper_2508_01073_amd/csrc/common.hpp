@@ -21,7 +21,7 @@ constexpr int kWave = 64;
   } while (0)
 #define RDF2V_LAUNCH_CHECK() RDF2V_HIP_TRY(hipGetLastError())
 
-inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+__host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Lane index inside the wavefront and the mask of lower lanes.
 __device__ __forceinline__ int lane_id() { return __lane_id(); }

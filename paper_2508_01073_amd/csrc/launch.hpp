@@ -69,4 +69,11 @@ rdf2v_status launch_unique_walks(const int32_t *tokens, const int32_t *len, int6
                                  int64_t *count_out, void *workspace, int32_t *status_dev,
                                  hipStream_t stream);
 
+size_t bfs_walks_workspace_bytes(int32_t num_entities, int64_t num_roots);
+rdf2v_status launch_bfs_walks(const int32_t *row_ptr, const int32_t *edges, int64_t num_edges,
+                              int32_t num_entities, int32_t num_predicates, const int32_t *roots,
+                              int64_t num_roots, int32_t depth, int32_t max_walks, int32_t *tokens_out,
+                              int32_t *len_out, int32_t *counts_out, void *workspace, int32_t *status_dev,
+                              hipStream_t stream);
+
 }  // namespace rdf2v

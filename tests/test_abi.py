@@ -33,7 +33,8 @@ def test_header_declares_the_calls():
     for n in ["rdf2v_build_csr", "rdf2v_build_csr_workspace_size", "rdf2v_random_walks", "rdf2v_build_walk_edges",
               "rdf2v_nonsink_starts", "rdf2v_nonsink_starts_workspace_size", "rdf2v_status_string",
               "rdf2v_skipgram_pairs", "rdf2v_skipgram_pairs_workspace_size", "rdf2v_random_walks_tokens",
-              "rdf2v_unique_walks", "rdf2v_unique_walks_workspace_size"]:
+              "rdf2v_unique_walks", "rdf2v_unique_walks_workspace_size", "rdf2v_bfs_walks",
+              "rdf2v_bfs_walks_workspace_size"]:
         assert n in names
 
 
@@ -202,6 +203,27 @@ def test_token_kind_and_unique_validation(lib):
     assert u(FAKE, FAKE, 100, 5, 9, None, FAKE, FAKE, WS, need, None, None) == E_INV
     assert u(FAKE, FAKE, 100, 5, 9, FAKE, FAKE, FAKE, None, need, None, None) == pkg.RDF2V_ERR_WORKSPACE
     assert u(FAKE, FAKE, 100, 5, 9, FAKE, FAKE, FAKE, WS, need - 1, None, None) == pkg.RDF2V_ERR_WORKSPACE
+
+
+def test_bfs_walks_validation(lib):
+    so, pkg = lib
+    c = _csr(pkg)
+    f = so.rdf2v_bfs_walks
+    need = pkg.rdf2v_bfs_walks_workspace_size(10, 5)
+    WS = ctypes.c_void_p(1 << 41)
+    E_INV = pkg.RDF2V_ERR_INVALID_ARGUMENT
+    assert f(None, FAKE, 5, 3, 4, FAKE, FAKE, FAKE, WS, need, None, None) == E_INV
+    assert f(ctypes.byref(c), FAKE, -1, 3, 4, FAKE, FAKE, FAKE, WS, need, None, None) == E_INV
+    assert f(ctypes.byref(c), FAKE, 5, 65, 4, FAKE, FAKE, FAKE, WS, need, None, None) == E_INV
+    assert f(ctypes.byref(c), FAKE, 5, 3, 0, FAKE, FAKE, FAKE, WS, need, None, None) == E_INV
+    assert f(ctypes.byref(c), None, 5, 3, 4, FAKE, FAKE, FAKE, WS, need, None, None) == E_INV
+    assert f(ctypes.byref(c), FAKE, 5, 3, 4, FAKE, FAKE, None, WS, need, None, None) == E_INV
+    assert f(ctypes.byref(c), FAKE, 5, 3, 4, FAKE, FAKE, FAKE, None, need, None, None) == pkg.RDF2V_ERR_WORKSPACE
+    assert f(ctypes.byref(c), FAKE, 5, 3, 4, FAKE, FAKE, FAKE, WS, need - 1, None, None) == pkg.RDF2V_ERR_WORKSPACE
+    assert f(ctypes.byref(c), FAKE, 2**40, 64, 4, FAKE, FAKE, FAKE, WS, need, None, None) == pkg.RDF2V_ERR_TOO_LARGE
+    assert f(ctypes.byref(c), FAKE, 0, 3, 4, None, None, None, None, 0, None, None) == pkg.RDF2V_OK
+    # the workspace is bounded (about 4 GiB) however many roots there are
+    assert pkg.rdf2v_bfs_walks_workspace_size(50_000_000, 10**7) <= (1 << 32) + 3 * 10**9
 
 
 def test_nonsink_argument_validation(lib):

@@ -1,0 +1,101 @@
+"""GPU parity for BFS walks (through the C ABI) against the oracle, bit-exact:
+hand-built graphs, random multigraphs and generated workloads, with depth
+limits, truncation at max_walks, sink and repeated roots."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2508_01073_amd as rd
+import synth
+from gpu_helpers import device, gpu_csr, new_status, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _compare(csr, rp, ed, V, P, roots, depth, max_walks, what, expect_capacity=None):
+    st = new_status()
+    tok, ln, cnt = rd.rdf2v_bfs_walks(csr, to_dev(roots), depth, max_walks, status=st)
+    torch.cuda.synchronize()
+    flags = int(st.item())
+    ref_t, ref_l, ref_c, trunc = oracle.bfs_walks(rp, ed, V, P, roots, depth, max_walks)
+    cnt = cnt.cpu().numpy()
+    assert np.array_equal(cnt, ref_c), f"{what}: walk counts differ"
+    tok = tok.cpu().numpy()
+    ln = ln.cpu().numpy()
+    for r in range(len(roots)):
+        k = ref_c[r]
+        if not (np.array_equal(tok[r, :k], ref_t[r, :k]) and np.array_equal(ln[r, :k], ref_l[r, :k])):
+            raise AssertionError(f"{what}: root {roots[r]} differs: gpu {tok[r, :k].tolist()[:3]} "
+                                 f"oracle {ref_t[r, :k].tolist()[:3]}")
+    assert bool(flags & rd.RDF2V_STATUS_CAPACITY) == (trunc > 0), what
+    assert not flags & ~rd.RDF2V_STATUS_CAPACITY, f"{what}: status {flags}"
+    return ref_c
+
+
+def test_hand_graphs():
+    say("[bfs] hand graphs")
+    tr = [(0, 0, 1), (0, 1, 2), (1, 0, 3), (2, 1, 3), (3, 0, 0)]
+    t = np.array(tr, np.int32)
+    rp, ed = oracle.build_csr(t[:, 0], t[:, 1], t[:, 2], 4, 2)
+    csr = gpu_csr(t[:, 0], t[:, 1], t[:, 2], 4, 2)
+    for depth in (0, 1, 2, 3, 5):
+        _compare(csr, rp, ed, 4, 2, np.array([0, 3, 2, 1, 0], np.int32), depth, 5, f"diamond depth {depth}")
+    star = np.array([(0, j % 2, j) for j in range(1, 12)] + [(5, 1, 0)], np.int32)
+    rp, ed = oracle.build_csr(star[:, 0], star[:, 1], star[:, 2], 12, 2)
+    csr = gpu_csr(star[:, 0], star[:, 1], star[:, 2], 12, 2)
+    _compare(csr, rp, ed, 12, 2, np.array([0, 7, 5], np.int32), 3, 4, "star truncated")
+    _compare(csr, rp, ed, 12, 2, np.array([0, 7, 5], np.int32), 3, 50, "star")
+
+
+@pytest.mark.parametrize("V,T,depth,seed", [(50, 150, 3, 0), (300, 1200, 4, 1), (2000, 6000, 6, 2),
+                                            (5000, 60_000, 2, 3), (40, 30, 10, 4)])
+def test_random_multigraphs(V, T, depth, seed):
+    say(f"[bfs] random multigraph V={V} T={T} depth={depth}")
+    P = 7
+    rng = np.random.default_rng(seed)
+    s = rng.integers(0, V, T).astype(np.int32)
+    p = rng.integers(0, P, T).astype(np.int32)
+    o = rng.integers(0, V, T).astype(np.int32)
+    s[:5] = 0; o[:2] = 0                        # self-loops and repeated edges at entity 0
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    roots = np.concatenate([np.arange(min(V, 600), dtype=np.int32), np.array([0, 0, V - 1], np.int32)])
+    _compare(csr, rp, ed, V, P, roots, depth, V, f"V={V} full")
+    _compare(csr, rp, ed, V, P, roots, depth, 7, f"V={V} truncated")
+
+
+def test_tiny_uniform_all_roots():
+    w = synth.WORKLOADS["tiny_uniform"]
+    say("[bfs] tiny_uniform, every entity as root, depth 3")
+    s, p, o = synth.triples(w)
+    V, P = w.num_entities, w.num_predicates
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    counts = _compare(csr, rp, ed, V, P, np.arange(V, dtype=np.int32), 3, 1000, "tiny_uniform")
+    assert counts.max() > 100
+
+
+def test_powerlaw_roots_with_hubs():
+    say("[bfs] power law 200k entities, depth 2, hub roots")
+    V, P = 200_000, 20
+    s, p, o = synth.powerlaw_triples(V, P, 2_000_000, sink_fraction=0.1)
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    deg = np.diff(rp)
+    hubs = np.argsort(-deg)[:8].astype(np.int32)
+    rng = np.random.default_rng(0)
+    roots = np.concatenate([hubs, rng.integers(0, V, 300).astype(np.int32)])
+    _compare(csr, rp, ed, V, P, roots, 2, 256, "power law hubs")
+
+
+def test_out_of_range_root_is_flagged():
+    say("[bfs] root out of range")
+    t = np.array([(0, 0, 1), (1, 0, 2)], np.int32)
+    csr = gpu_csr(t[:, 0], t[:, 1], t[:, 2], 3, 1)
+    st = new_status()
+    tok, ln, cnt = rd.rdf2v_bfs_walks(csr, to_dev([0, 9, 1]), 2, 4, status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) & rd.RDF2V_STATUS_ID_OUT_OF_RANGE
+    assert cnt.cpu().tolist() == [1, 0, 1]
