@@ -76,6 +76,8 @@ def _load():
     lib.rdf2v_ref_bfs_walks.argtypes = [i32p, i32p, ctypes.c_int32, ctypes.c_int32, i32p, ctypes.c_int64,
                                         ctypes.c_int32, ctypes.c_int32, i32p, i32p, i32p]
     lib.rdf2v_ref_bfs_walks.restype = ctypes.c_int64
+    lib.rdf2v_ref_build_vocabulary.argtypes = [i32p] * 6 + [ctypes.c_int64] + [i32p] * 5
+    lib.rdf2v_ref_build_vocabulary.restype = ctypes.c_int
     lib.rdf2v_ref_skipgram_pairs.argtypes = [i32p, i32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                              i32p, ctypes.c_int64]
     lib.rdf2v_ref_skipgram_pairs.restype = ctypes.c_int64
@@ -240,3 +242,22 @@ def bfs_walks(row_ptr, edges, num_entities: int, num_predicates: int, roots, dep
     if k < 0:
         raise OracleError(int(-k), "rdf2v_ref_bfs_walks")
     return tokens, lens, counts, int(k)
+
+
+def build_vocabulary(subj_chars, subj_off, pred_chars, pred_off, obj_chars, obj_off):
+    """String triples (uint8 char buffers + int64 offsets per column) -> (subj_ids, pred_ids,
+    obj_ids, num_entities, num_predicates); ids in order of first appearance (entities over
+    s0, o0, s1, o1, ...; predicates over p0, p1, ...)."""
+    lib = _load()
+    cols = [np.ascontiguousarray(a) for a in (subj_chars, subj_off, pred_chars, pred_off, obj_chars, obj_off)]
+    for c in cols[1::2]:
+        assert c.dtype == np.int64
+    T = cols[1].shape[0] - 1
+    ids = [np.empty(T, dtype=np.int32) for _ in range(3)]
+    ne = np.zeros(1, np.int64)
+    npred = np.zeros(1, np.int64)
+    ptr = lambda a: ctypes.c_void_p(a.ctypes.data)
+    st = lib.rdf2v_ref_build_vocabulary(*[ptr(c) for c in cols], T, *[ptr(i) for i in ids], ptr(ne), ptr(npred))
+    if st != OK:
+        raise OracleError(st, "rdf2v_ref_build_vocabulary")
+    return ids[0], ids[1], ids[2], int(ne[0]), int(npred[0])

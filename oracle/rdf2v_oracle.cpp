@@ -30,10 +30,17 @@
 // parity pinned: Philox against rocRAND's host-callable Philox4x32-10, the edge
 // index against its closed form, the CSR against std::stable_sort / numpy's
 // stable argsort, and the walks against chain, sink, brute-force-enumeration and
-// chi-square uniformity tests (see tests/test_oracle_pins.py).
+// chi-square uniformity tests (see tests/test_oracle_pins.py); skip-gram pairs,
+// entity/property walks and duplicate-free walks against hand-worked examples,
+// independent numpy constructions and closed-form counts
+// (tests/test_oracle_pairs.py); BFS walks against scipy's breadth_first_order
+// (tests/test_oracle_bfs.py); the vocabulary against pandas.factorize and the
+// integer graph its strings were made from (tests/test_oracle_vocab.py).
 
 #include <cstdint>
 #include <cstddef>
+#include <string>
+#include <unordered_map>
 #include <vector>
 
 namespace {
@@ -339,6 +346,37 @@ int64_t rdf2v_ref_bfs_walks(const int32_t *row_ptr, const int32_t *edges, int32_
   }
   (void)num_predicates;
   return truncated;
+}
+
+// Vocabulary (Sec. 3.1: every entity and predicate is tokenised to an integer
+// id at the start of the pipeline). Strings are given as byte buffers with
+// offsets (string i is chars[offsets[i] .. offsets[i+1])). Entity ids number
+// the distinct subject and object strings in order of first appearance over
+// s_0, o_0, s_1, o_1, ...; predicate ids number the distinct predicate strings
+// in order of first appearance over p_0, p_1, .... Returns 0, or an error code.
+int rdf2v_ref_build_vocabulary(const char *s_chars, const int64_t *s_off, const char *p_chars,
+                               const int64_t *p_off, const char *o_chars, const int64_t *o_off,
+                               int64_t num_triples, int32_t *s_ids, int32_t *p_ids, int32_t *o_ids,
+                               int64_t *num_entities, int64_t *num_predicates) {
+  if (num_triples < 0) return REF_ERR_INVALID_ARGUMENT;
+  std::unordered_map<std::string, int32_t> entities, predicates;
+  auto id_of = [](std::unordered_map<std::string, int32_t> &vocab, const char *chars, const int64_t *off,
+                  int64_t i) {
+    const std::string key(chars + off[i], size_t(off[i + 1] - off[i]));
+    auto it = vocab.find(key);
+    if (it != vocab.end()) return it->second;
+    const int32_t id = int32_t(vocab.size());
+    vocab.emplace(key, id);
+    return id;
+  };
+  for (int64_t t = 0; t < num_triples; ++t) {
+    s_ids[t] = id_of(entities, s_chars, s_off, t);
+    o_ids[t] = id_of(entities, o_chars, o_off, t);
+    p_ids[t] = id_of(predicates, p_chars, p_off, t);
+  }
+  *num_entities = int64_t(entities.size());
+  *num_predicates = int64_t(predicates.size());
+  return REF_OK;
 }
 
 // Skip-gram training pairs (Sec. 3.2: the data module turns the walk corpus

@@ -91,6 +91,9 @@ def _load():
                                    ctypes.c_double, ctypes.c_double, ctypes.c_double, vp, vp, vp,
                                    vp, vp, ctypes.c_int]
     lib.synth_powerlaw.restype = ctypes.c_int
+    lib.synth_label_column.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int64, ctypes.c_char_p,
+                                       ctypes.c_int32, vp, vp, vp, ctypes.c_int]
+    lib.synth_label_column.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -139,3 +142,43 @@ def triples(workload: Workload | str, seed: int = GENERATOR_SEED):
         return uniform_triples(w.num_entities, w.num_predicates, w.num_triples, seed)
     return powerlaw_triples(w.num_entities, w.num_predicates, w.num_triples, w.gamma, w.pred_s,
                             w.sink_fraction, seed)
+
+
+# ----------------------------------------------------------------------------
+# String form of a graph: IRI-like labels for entities and predicates
+# ----------------------------------------------------------------------------
+
+ENTITY_PREFIX = b"http://kg.example.org/entity/Q"
+PREDICATE_PREFIX = b"http://kg.example.org/relation/P"
+
+
+def label_column(ids, labels, prefix: bytes):
+    """String column (chars uint8, offsets int64 with len(ids) + 1 entries): string t is
+    ``prefix`` followed by the decimal digits of ``labels[ids[t]]``."""
+    lib = _load()
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    labels = np.ascontiguousarray(labels, dtype=np.int64)
+    n = ids.shape[0]
+    lens = np.empty(n, dtype=np.int64)
+    rc = lib.synth_label_column(ids.ctypes.data, n, labels.ctypes.data, labels.shape[0], prefix,
+                                len(prefix), lens.ctypes.data, None, None, _threads())
+    if rc != 0:
+        raise ValueError("label_column: id out of range")
+    offsets = np.zeros(n + 1, dtype=np.int64)
+    np.cumsum(lens, out=offsets[1:])
+    del lens
+    chars = np.empty(int(offsets[-1]), dtype=np.uint8)
+    lib.synth_label_column(ids.ctypes.data, n, labels.ctypes.data, labels.shape[0], prefix, len(prefix),
+                           None, offsets.ctypes.data, chars.ctypes.data, _threads())
+    return chars, offsets
+
+
+def string_triples(s, p, o, num_entities: int, num_predicates: int, seed: int = GENERATOR_SEED):
+    """The string form of id triples: every entity and predicate id gets a distinct IRI-like
+    label, numbered by a seeded random bijection (so label order is unrelated to id order).
+    Returns ((s_chars, s_off), (p_chars, p_off), (o_chars, o_off))."""
+    rng = np.random.default_rng([seed, 7])
+    ent = rng.permutation(num_entities).astype(np.int64) + 1
+    prd = rng.permutation(num_predicates).astype(np.int64) + 1
+    return (label_column(s, ent, ENTITY_PREFIX), label_column(p, prd, PREDICATE_PREFIX),
+            label_column(o, ent, ENTITY_PREFIX))

@@ -197,4 +197,42 @@ int synth_powerlaw(uint64_t seed, int64_t num_triples, int32_t num_entities, int
   return 0;
 }
 
+// Text columns for the string form of a triple column: string t is prefix
+// followed by the decimal digits of label[ids[t]]. With chars == nullptr only
+// the byte lengths are written (to lens); otherwise offsets (n + 1 entries,
+// their prefix sum) locate string t at chars[offsets[t] ..).
+int synth_label_column(const int32_t *ids, int64_t n, const int64_t *label, int64_t num_labels,
+                       const char *prefix, int32_t prefix_len, int64_t *lens, const int64_t *offsets,
+                       uint8_t *chars, int nthreads) {
+  if (n < 0 || prefix_len < 0) return 1;
+  auto digits = [](int64_t x, char *buf) {
+    int k = 0;
+    do {
+      buf[k++] = char('0' + x % 10);
+      x /= 10;
+    } while (x > 0);
+    return k;
+  };
+  int bad = 0;
+  parallel_for(n, nthreads, [&](int64_t lo, int64_t hi) {
+    char buf[24];
+    for (int64_t t = lo; t < hi; ++t) {
+      const int32_t id = ids[t];
+      if (id < 0 || id >= num_labels || label[id] < 0) {
+        bad = 1;
+        continue;
+      }
+      const int k = digits(label[id], buf);
+      if (chars == nullptr) {
+        lens[t] = prefix_len + k;
+        continue;
+      }
+      uint8_t *dst = chars + offsets[t];
+      for (int32_t j = 0; j < prefix_len; ++j) dst[j] = uint8_t(prefix[j]);
+      for (int j = 0; j < k; ++j) dst[prefix_len + j] = uint8_t(buf[k - 1 - j]);
+    }
+  });
+  return bad;
+}
+
 }  // extern "C"
