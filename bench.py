@@ -214,6 +214,41 @@ def time_unique(rd, torch, tokens, lens, n_walks, batch_cap, wpn, stream, ev):
             "frac_of_hbm_peak": useful / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
 
 
+def time_vocab(rd, torch, synth, w, s, p, o, stream, ev):
+    """Time rdf2v_build_vocabulary on the string form of the workload's triples (IRI-like
+    labels, a seeded bijection of the ids). Streaming bytes: every string byte and offset
+    read once and every id written once (the hash-table probes are not counted)."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    cols = synth.string_triples(s, p, o, w.num_entities, w.num_predicates)
+    dcols = [(torch.from_numpy(c).to(dev), torch.from_numpy(off).to(dev)) for c, off in cols]
+    T = int(s.shape[0])
+    ids = tuple(torch.empty(T, dtype=torch.int32, device=dev) for _ in range(3))
+    counts = torch.empty(2, dtype=torch.int64, device=dev)
+    ws = torch.empty(rd.rdf2v_build_vocabulary_workspace_size(T, w.num_entities, w.num_predicates),
+                     dtype=torch.uint8, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    call = lambda: rd.rdf2v_build_vocabulary(*dcols, w.num_entities, w.num_predicates, ids=ids, counts=counts,
+                                             workspace=ws, status=status, stream=stream)
+    call()
+    torch.cuda.synchronize()
+    rd.check_device_status(status, "vocabulary")
+    e0, e1 = ev(), ev()
+    e0.record(stream)
+    for _ in range(3):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 3
+    chars = sum(int(c.nbytes) for c, _ in cols)
+    streamed = chars + 3 * 8 * (T + 1) + 3 * 4 * T
+    ne, npred = [int(x) for x in counts.cpu()]
+    return {"triples": T, "string_bytes": chars, "distinct_entities": ne, "distinct_predicates": npred,
+            "ms": ms, "triples_per_s": T / (ms * 1e-3), "string_GBps": chars / (ms * 1e-3) / 1e9,
+            "streamed_GBps": streamed / (ms * 1e-3) / 1e9,
+            "frac_of_hbm_peak": streamed / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -233,6 +268,9 @@ def main() -> int:
                     help="also time skip-gram pair generation over the corpus with this window "
                          "(0: off)")
     ap.add_argument("--pairs-batch-walks", type=int, default=8_000_000)
+    ap.add_argument("--vocab", action="store_true",
+                    help="also time the vocabulary (string triples -> ids) on IRI-like labels of "
+                         "the workload's triples")
     ap.add_argument("--copy-probe-mib", type=int, default=1024,
                     help="size of the plain device copy timed first (bandwidth reference, "
                          "counter calibration)")
@@ -401,6 +439,8 @@ def main() -> int:
     if args.pairs_window > 0:
         out["skipgram_pairs"] = time_pairs(rd, torch, tokens, lens, n_walks, batch_cap, width,
                                            args.pairs_window, args.pairs_batch_walks, stream, ev)
+    if args.vocab:
+        out["vocabulary"] = time_vocab(rd, torch, synth, w, s, p, o, stream, ev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, s, p, o, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -52,8 +52,8 @@ typedef enum rdf2v_status {
 /* Bits ORed into *status_dev by the kernels. */
 #define RDF2V_STATUS_ID_OUT_OF_RANGE 0x1 /* a subject/object/start id >= num_entities or < 0, or a predicate id out of range */
 #define RDF2V_STATUS_BAD_CSR 0x2         /* row_ptr not non-decreasing within [0, num_edges] */
-#define RDF2V_STATUS_BAD_LENGTH 0x4      /* a walk length outside [0, row_width] (treated as clamped) */
-#define RDF2V_STATUS_CAPACITY 0x8        /* more pairs than the output holds (the rest are not written) */
+#define RDF2V_STATUS_BAD_LENGTH 0x4      /* a walk length outside [0, row_width] (treated as clamped), or a bad string offset */
+#define RDF2V_STATUS_CAPACITY 0x8        /* more results than the output holds (the rest are not written), or more distinct strings than a vocabulary bound */
 
 /* Longest walk, in hops. A walk row holds 2 * depth + 1 tokens. */
 #define RDF2V_MAX_DEPTH 64
@@ -290,6 +290,54 @@ size_t rdf2v_bfs_walks_workspace_size(int32_t num_entities, int64_t num_roots);
 rdf2v_status rdf2v_bfs_walks(const rdf2v_csr *csr, const int32_t *roots, int64_t num_roots, int32_t depth,
                              int32_t max_walks, int32_t *tokens_out, int32_t *len_out, int32_t *counts_out,
                              void *workspace, size_t workspace_bytes, int32_t *status_dev, void *stream);
+
+/* Largest num_triples and bound on distinct strings rdf2v_build_vocabulary takes. */
+#define RDF2V_VOCAB_MAX_TRIPLES ((int64_t)1 << 30)
+#define RDF2V_VOCAB_MAX_DISTINCT ((int64_t)1 << 30)
+
+/* Bytes of device workspace rdf2v_build_vocabulary needs (0 for arguments it
+ * rejects). Pure host function. */
+size_t rdf2v_build_vocabulary_workspace_size(int64_t num_triples, int64_t max_entities, int64_t max_predicates);
+
+/*
+ * Vocabulary (gpuRDF2vec Sec. 3.1: every entity and predicate is tokenised to
+ * an integer id at the start of the pipeline): string triples -> the int32 id
+ * triples that rdf2v_build_csr takes.
+ *
+ * Entity ids number the distinct subject and object strings 0, 1, ... in the
+ * order they first appear in s_0, o_0, s_1, o_1, ...; predicate ids number the
+ * distinct predicate strings in the order they first appear in p_0, p_1, ....
+ * Strings are compared as byte sequences (any bytes, NUL included; the empty
+ * string is a string). The result is deterministic.
+ *
+ * Each column is given as
+ *   X_chars     uint8 bytes of all strings of the column (device), 4-byte
+ *               aligned; may be NULL when X_bytes == 0.
+ *   X_offsets   [num_triples + 1] int64 (device): string t of the column is
+ *               X_chars[X_offsets[t] .. X_offsets[t + 1]). Offsets outside
+ *               [0, X_bytes] or decreasing raise RDF2V_STATUS_BAD_LENGTH (the
+ *               string is then read as empty).
+ *   X_bytes     length of X_chars in bytes (nothing past it is read).
+ * for X = subj, pred, obj.
+ *
+ *   num_triples     0 .. RDF2V_VOCAB_MAX_TRIPLES.
+ *   max_entities,   caller's upper bounds on the distinct entity and predicate
+ *   max_predicates  strings, 1 .. RDF2V_VOCAB_MAX_DISTINCT; they size the hash
+ *                   tables (2 to 4 x the bound, 16 B a slot). More distinct
+ *                   strings than a bound raise RDF2V_STATUS_CAPACITY.
+ *   subj_ids, pred_ids, obj_ids  [num_triples] int32 outputs (device).
+ *   counts_out      [2] int64 (device): distinct entities, distinct predicates.
+ *   workspace       rdf2v_build_vocabulary_workspace_size(num_triples,
+ *                   max_entities, max_predicates) bytes, 256-byte aligned.
+ *   status_dev      device int32 or NULL (RDF2V_STATUS_BAD_LENGTH,
+ *                   RDF2V_STATUS_CAPACITY).
+ */
+rdf2v_status rdf2v_build_vocabulary(const uint8_t *subj_chars, const int64_t *subj_offsets, int64_t subj_bytes,
+                                    const uint8_t *pred_chars, const int64_t *pred_offsets, int64_t pred_bytes,
+                                    const uint8_t *obj_chars, const int64_t *obj_offsets, int64_t obj_bytes,
+                                    int64_t num_triples, int64_t max_entities, int64_t max_predicates,
+                                    int32_t *subj_ids, int32_t *pred_ids, int32_t *obj_ids, int64_t *counts_out,
+                                    void *workspace, size_t workspace_bytes, int32_t *status_dev, void *stream);
 
 /* Static, human-readable name of a status code. */
 const char *rdf2v_status_string(rdf2v_status status);

@@ -29,7 +29,8 @@ __all__ = [
     "rdf2v_nonsink_starts", "rdf2v_random_walks", "rdf2v_random_walks_tokens",
     "rdf2v_unique_walks_workspace_size", "rdf2v_unique_walks", "rdf2v_bfs_walks_workspace_size",
     "rdf2v_bfs_walks", "rdf2v_skipgram_pairs_workspace_size",
-    "rdf2v_skipgram_pairs", "rdf2v_status_string", "check_device_status",
+    "rdf2v_skipgram_pairs", "rdf2v_build_vocabulary_workspace_size", "rdf2v_build_vocabulary",
+    "rdf2v_status_string", "check_device_status",
     "library_path",
 ]
 
@@ -99,6 +100,10 @@ def _native():
     lib.rdf2v_skipgram_pairs_workspace_size.restype = sz
     lib.rdf2v_skipgram_pairs.argtypes = [vp, vp, i64, i32, i32, vp, i64, vp, vp, sz, vp, vp]
     lib.rdf2v_skipgram_pairs.restype = ctypes.c_int
+    lib.rdf2v_build_vocabulary_workspace_size.argtypes = [i64, i64, i64]
+    lib.rdf2v_build_vocabulary_workspace_size.restype = sz
+    lib.rdf2v_build_vocabulary.argtypes = [vp, vp, i64] * 3 + [i64, i64, i64, vp, vp, vp, vp, vp, sz, vp, vp]
+    lib.rdf2v_build_vocabulary.restype = ctypes.c_int
     lib.rdf2v_status_string.argtypes = [ctypes.c_int]
     lib.rdf2v_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -378,6 +383,51 @@ def rdf2v_skipgram_pairs(tokens: torch.Tensor, lens: torch.Tensor, window: int, 
     out = torch.empty((n, 2), dtype=torch.int32, device=dev)
     call(out, n)
     return out
+
+
+def rdf2v_build_vocabulary_workspace_size(num_triples: int, max_entities: int, max_predicates: int) -> int:
+    return int(_native().rdf2v_build_vocabulary_workspace_size(num_triples, max_entities, max_predicates))
+
+
+def _string_column(col, name: str, n: int):
+    chars, offsets = col
+    for t, dt in ((chars, torch.uint8), (offsets, torch.int64)):
+        if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+            raise TypeError(f"{name} must be CUDA (HIP) tensors")
+        if t.dtype != dt or not t.is_contiguous():
+            raise TypeError(f"{name}: chars must be contiguous uint8 and offsets contiguous int64")
+    if offsets.shape[0] != n + 1:
+        raise ValueError(f"{name}: offsets must hold num_triples + 1 entries")
+    return [_ptr(chars), _ptr(offsets), int(chars.numel())]
+
+
+def rdf2v_build_vocabulary(subj, pred, obj, max_entities: int, max_predicates: int, *,
+                           ids: tuple | None = None, counts: torch.Tensor | None = None,
+                           workspace: torch.Tensor | None = None, status: torch.Tensor | None = None,
+                           stream=None):
+    """String triples -> id triples. subj, pred, obj are (chars uint8, offsets int64) device
+    tensor pairs, string t of a column being chars[offsets[t]:offsets[t+1]].
+
+    Returns (subj_ids, pred_ids, obj_ids, counts): int32 [T] each and a device int64 [2] of
+    (distinct entities, distinct predicates); no host synchronisation."""
+    offsets = subj[1]
+    dev = offsets.device
+    n = int(offsets.shape[0]) - 1
+    args = (_string_column(subj, "subj", n) + _string_column(pred, "pred", n) + _string_column(obj, "obj", n))
+    if ids is None:
+        ids = tuple(torch.empty(n, dtype=torch.int32, device=dev) for _ in range(3))
+    for i, name in zip(ids, ("subj_ids", "pred_ids", "obj_ids")):
+        _dev_i32(i, name)
+    if counts is None:
+        counts = torch.empty(2, dtype=torch.int64, device=dev)
+    if workspace is None:
+        need = rdf2v_build_vocabulary_workspace_size(n, max_entities, max_predicates)
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = _native().rdf2v_build_vocabulary(*args, n, max_entities, max_predicates, *[_ptr(i) for i in ids],
+                                          _ptr(counts), _ptr(workspace), workspace.numel(), _ptr(status),
+                                          _stream(dev, stream))
+    _check(st, "rdf2v_build_vocabulary")
+    return ids[0], ids[1], ids[2], counts
 
 
 def check_device_status(status: torch.Tensor, where: str = "device") -> None:

@@ -216,6 +216,59 @@ RDF2V_API rdf2v_status rdf2v_bfs_walks(const rdf2v_csr *csr, const int32_t *root
                                  counts_out, workspace, status_dev, static_cast<hipStream_t>(stream));
 }
 
+namespace {
+
+bool vocab_sizes_ok(int64_t num_triples, int64_t max_entities, int64_t max_predicates) {
+  return num_triples >= 0 && num_triples <= RDF2V_VOCAB_MAX_TRIPLES && max_entities >= 1 &&
+         max_entities <= RDF2V_VOCAB_MAX_DISTINCT && max_predicates >= 1 &&
+         max_predicates <= RDF2V_VOCAB_MAX_DISTINCT;
+}
+
+bool column_ok(const uint8_t *chars, const int64_t *offsets, int64_t bytes, int64_t num_triples) {
+  if (bytes < 0) return false;
+  if (num_triples > 0 && offsets == nullptr) return false;
+  if (bytes > 0 && chars == nullptr) return false;
+  return (reinterpret_cast<uintptr_t>(chars) & 3) == 0;
+}
+
+}  // namespace
+
+RDF2V_API size_t rdf2v_build_vocabulary_workspace_size(int64_t num_triples, int64_t max_entities,
+                                                       int64_t max_predicates) {
+  if (!vocab_sizes_ok(num_triples, max_entities, max_predicates)) return 0;
+  return rdf2v::vocabulary_workspace_bytes(num_triples, max_entities, max_predicates);
+}
+
+RDF2V_API rdf2v_status rdf2v_build_vocabulary(const uint8_t *subj_chars, const int64_t *subj_offsets,
+                                              int64_t subj_bytes, const uint8_t *pred_chars,
+                                              const int64_t *pred_offsets, int64_t pred_bytes,
+                                              const uint8_t *obj_chars, const int64_t *obj_offsets,
+                                              int64_t obj_bytes, int64_t num_triples, int64_t max_entities,
+                                              int64_t max_predicates, int32_t *subj_ids, int32_t *pred_ids,
+                                              int32_t *obj_ids, int64_t *counts_out, void *workspace,
+                                              size_t workspace_bytes, int32_t *status_dev, void *stream) {
+  if (num_triples > RDF2V_VOCAB_MAX_TRIPLES || max_entities > RDF2V_VOCAB_MAX_DISTINCT ||
+      max_predicates > RDF2V_VOCAB_MAX_DISTINCT)
+    return RDF2V_ERR_TOO_LARGE;
+  if (!vocab_sizes_ok(num_triples, max_entities, max_predicates) || counts_out == nullptr)
+    return RDF2V_ERR_INVALID_ARGUMENT;
+  if (!column_ok(subj_chars, subj_offsets, subj_bytes, num_triples) ||
+      !column_ok(pred_chars, pred_offsets, pred_bytes, num_triples) ||
+      !column_ok(obj_chars, obj_offsets, obj_bytes, num_triples))
+    return RDF2V_ERR_INVALID_ARGUMENT;
+  if (num_triples > 0 && (subj_ids == nullptr || pred_ids == nullptr || obj_ids == nullptr))
+    return RDF2V_ERR_INVALID_ARGUMENT;
+  const size_t need = rdf2v::vocabulary_workspace_bytes(num_triples, max_entities, max_predicates);
+  if (workspace == nullptr || workspace_bytes < need) return RDF2V_ERR_WORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return RDF2V_ERR_WORKSPACE;
+  const rdf2v::VocabColumns cols{{subj_chars, pred_chars, obj_chars},
+                                 {subj_offsets, pred_offsets, obj_offsets},
+                                 {subj_bytes, pred_bytes, obj_bytes}};
+  return rdf2v::launch_build_vocabulary(cols, num_triples, max_entities, max_predicates, subj_ids, pred_ids,
+                                        obj_ids, counts_out, workspace, status_dev,
+                                        static_cast<hipStream_t>(stream));
+}
+
 RDF2V_API const char *rdf2v_status_string(rdf2v_status status) {
   switch (status) {
     case RDF2V_OK: return "RDF2V_OK";

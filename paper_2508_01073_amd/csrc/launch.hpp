@@ -76,4 +76,17 @@ rdf2v_status launch_bfs_walks(const int32_t *row_ptr, const int32_t *edges, int6
                               int32_t *len_out, int32_t *counts_out, void *workspace, int32_t *status_dev,
                               hipStream_t stream);
 
+// The three string columns of rdf2v_build_vocabulary, in the order subject,
+// predicate, object.
+struct VocabColumns {
+  const uint8_t *chars[3];
+  const int64_t *offsets[3];
+  int64_t bytes[3];
+};
+size_t vocabulary_workspace_bytes(int64_t num_triples, int64_t max_entities, int64_t max_predicates);
+rdf2v_status launch_build_vocabulary(const VocabColumns &cols, int64_t num_triples, int64_t max_entities,
+                                     int64_t max_predicates, int32_t *subj_ids, int32_t *pred_ids,
+                                     int32_t *obj_ids, int64_t *counts_out, void *workspace,
+                                     int32_t *status_dev, hipStream_t stream);
+
 }  // namespace rdf2v

@@ -34,7 +34,8 @@ def test_header_declares_the_calls():
               "rdf2v_nonsink_starts", "rdf2v_nonsink_starts_workspace_size", "rdf2v_status_string",
               "rdf2v_skipgram_pairs", "rdf2v_skipgram_pairs_workspace_size", "rdf2v_random_walks_tokens",
               "rdf2v_unique_walks", "rdf2v_unique_walks_workspace_size", "rdf2v_bfs_walks",
-              "rdf2v_bfs_walks_workspace_size"]:
+              "rdf2v_bfs_walks_workspace_size", "rdf2v_build_vocabulary",
+              "rdf2v_build_vocabulary_workspace_size"]:
         assert n in names
 
 
@@ -224,6 +225,41 @@ def test_bfs_walks_validation(lib):
     assert f(ctypes.byref(c), FAKE, 0, 3, 4, None, None, None, None, 0, None, None) == pkg.RDF2V_OK
     # the workspace is bounded (about 4 GiB) however many roots there are
     assert pkg.rdf2v_bfs_walks_workspace_size(50_000_000, 10**7) <= (1 << 32) + 3 * 10**9
+
+
+def test_vocabulary_validation(lib):
+    so, pkg = lib
+    f = so.rdf2v_build_vocabulary
+    T, ME, MP = 100, 50, 10
+    need = pkg.rdf2v_build_vocabulary_workspace_size(T, ME, MP)
+    assert need > 0
+    WS = ctypes.c_void_p(1 << 41)
+    E_INV = pkg.RDF2V_ERR_INVALID_ARGUMENT
+    col = [FAKE, FAKE, 4000]
+
+    def call(cols=None, t=T, me=ME, mp=MP, ids=(FAKE, FAKE, FAKE), counts=FAKE, ws=WS, nbytes=None):
+        cols = cols or [col, col, col]
+        return f(*cols[0], *cols[1], *cols[2], t, me, mp, *ids, counts, ws, need if nbytes is None else nbytes,
+                 None, None)
+
+    assert call(t=-1) == E_INV
+    assert call(me=0) == E_INV and call(mp=0) == E_INV
+    assert call(t=(1 << 30) + 1) == pkg.RDF2V_ERR_TOO_LARGE
+    assert call(me=(1 << 30) + 1) == pkg.RDF2V_ERR_TOO_LARGE
+    assert call(counts=None) == E_INV
+    assert call(ids=(FAKE, None, FAKE)) == E_INV
+    assert call(cols=[col, [FAKE, None, 4000], col]) == E_INV                  # offsets missing
+    assert call(cols=[col, col, [None, FAKE, 4000]]) == E_INV                  # chars missing
+    assert call(cols=[[ctypes.c_void_p((1 << 40) + 2), FAKE, 4000], col, col]) == E_INV  # chars unaligned
+    assert call(cols=[col, [FAKE, FAKE, -1], col]) == E_INV
+    assert call(ws=None) == pkg.RDF2V_ERR_WORKSPACE
+    assert call(nbytes=need - 1) == pkg.RDF2V_ERR_WORKSPACE
+    assert call(ws=ctypes.c_void_p((1 << 41) + 16)) == pkg.RDF2V_ERR_WORKSPACE
+    # the tables are sized from the bounds: 2 to 4 slots of 16 B per distinct string
+    small = pkg.rdf2v_build_vocabulary_workspace_size(10**6, 1000, 10)
+    big = pkg.rdf2v_build_vocabulary_workspace_size(10**6, 10**6, 10)
+    assert 2 * 16 * (10**6 - 1000) <= big - small <= 4 * 16 * 10**6
+    assert pkg.rdf2v_build_vocabulary_workspace_size(-1, 1, 1) == 0
 
 
 def test_nonsink_argument_validation(lib):

@@ -1,0 +1,229 @@
+"""GPU parity for the vocabulary (rdf2v_build_vocabulary, through the C ABI)
+against the oracle, bit-exact: hand-worked strings, near-duplicate byte
+strings at every alignment, strings whose hash tags collide, the generated
+workloads' IRI columns, bounds, bad offsets, and the string pipeline end to
+end (vocabulary -> CSR -> walks)."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2508_01073_amd as rd
+import synth
+from gpu_helpers import device, new_status, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _column(strings, lead=0):
+    """(chars, offsets) for a list of byte strings; `lead` junk bytes come first, so
+    that the strings start at other alignments."""
+    data = [s.encode() if isinstance(s, str) else s for s in strings]
+    off = np.zeros(len(data) + 1, np.int64)
+    off[1:] = np.cumsum([len(d) for d in data])
+    body = b"".join(data)
+    chars = np.frombuffer(b"\xab" * lead + body, np.uint8).copy()
+    return chars, off + lead
+
+
+def _dev_col(col):
+    chars, off = col
+    return (torch.from_numpy(np.ascontiguousarray(chars, np.uint8)).to(device()),
+            torch.from_numpy(np.ascontiguousarray(off, np.int64)).to(device()))
+
+
+def _run(cols, max_e, max_p, status=None, stream=None):
+    st = new_status() if status is None else status
+    s, p, o, counts = rd.rdf2v_build_vocabulary(*[_dev_col(c) for c in cols], max_e, max_p, status=st,
+                                                stream=stream)
+    torch.cuda.synchronize()
+    return (s.cpu().numpy(), p.cpu().numpy(), o.cpu().numpy(), counts.cpu().numpy().tolist(),
+            int(st.item()))
+
+
+def _compare(cols, what, max_e=None, max_p=None):
+    ref = oracle.build_vocabulary(cols[0][0], cols[0][1], cols[1][0], cols[1][1], cols[2][0], cols[2][1])
+    T = len(cols[0][1]) - 1
+    max_e = max_e or max(1, 2 * T)
+    max_p = max_p or max(1, T)
+    s, p, o, counts, flags = _run(cols, max_e, max_p)
+    assert flags == 0, f"{what}: status {flags}"
+    assert counts == [ref[3], ref[4]], f"{what}: counts {counts} vs {ref[3:]}"
+    for name, got, exp in (("subj", s, ref[0]), ("pred", p, ref[1]), ("obj", o, ref[2])):
+        if not np.array_equal(got, exp):
+            bad = np.nonzero(got != exp)[0]
+            raise AssertionError(f"{what}: {name} ids differ at {bad.size} rows, first {bad[:5].tolist()}: "
+                                 f"gpu {got[bad[:5]].tolist()} oracle {exp[bad[:5]].tolist()}")
+    return ref
+
+
+def test_hand_worked():
+    say("[vocab] hand-worked")
+    S = ["b", "a", "b", "", "ab"]
+    P = ["knows", "knows", "likes", "a", "knows"]
+    O = ["a", "c", "b", "a", "a\x00"]
+    for lead in range(4):
+        ref = _compare([_column(S, lead), _column(P, 3 - lead), _column(O, lead)], f"hand lead={lead}")
+    assert ref[0].tolist() == [0, 1, 0, 3, 4] and ref[2].tolist() == [1, 2, 0, 1, 5]
+
+
+def test_empty_and_single():
+    say("[vocab] empty and single")
+    e = _column([])
+    s, p, o, counts, flags = _run([e, e, e], 1, 1)
+    assert s.size == 0 and counts == [0, 0] and flags == 0
+    _compare([_column([""]), _column([""]), _column([""])], "single empty strings")
+    _compare([_column(["x"]), _column(["x"]), _column(["x"])], "single")
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_near_duplicates_every_alignment(seed):
+    say(f"[vocab] near duplicates seed={seed}")
+    rng = np.random.default_rng(seed)
+    alphabet = [b"a", b"b", b"\x00", b"\xff"]
+    short = [b"".join(rng.choice(alphabet, size=int(rng.integers(0, 9)))) for _ in range(400)]
+    stem = bytes(rng.integers(0, 256, 300, dtype=np.uint8))
+    long = [stem[:int(k)] + bytes([int(b)]) for k, b in zip(rng.integers(0, 300, 200), rng.integers(0, 3, 200))]
+    pool = short + long
+    T = 3000
+    cols = [_column([pool[i] for i in rng.integers(0, len(pool), T)], lead=int(rng.integers(0, 8)))
+            for _ in range(3)]
+    _compare(cols, f"near duplicates seed={seed}")
+    # bounds equal to the exact distinct counts are enough
+    ref = oracle.build_vocabulary(cols[0][0], cols[0][1], cols[1][0], cols[1][1], cols[2][0], cols[2][1])
+    _compare(cols, "exact bounds", max_e=ref[3], max_p=ref[4])
+
+
+def _np_hash(strings):
+    """The library's 64-bit string hash, restated in numpy for equal-length strings
+    (used only to construct strings whose hash tags collide)."""
+    M = (1 << 64) - 1
+    n = len(strings[0])
+    a = np.frombuffer(b"".join(strings), np.uint8).reshape(len(strings), n)
+    pad = (-n) % 4
+    a = np.concatenate([a, np.zeros((len(strings), pad), np.uint8)], axis=1)
+    chunks = a.view("<u4").astype(np.uint64)
+    with np.errstate(over="ignore"):
+        h = np.full(len(strings), np.uint64(0x243f6a8885a308d3 ^ ((n * 0x9e3779b97f4a7c15) & M)))
+        for k in range(chunks.shape[1]):
+            h = (h ^ chunks[:, k]) * np.uint64(0x100000001b3)
+            h ^= h >> np.uint64(29)
+        h ^= h >> np.uint64(33)
+        h *= np.uint64(0xff51afd7ed558ccd)
+        h ^= h >> np.uint64(33)
+        h *= np.uint64(0xc4ceb9fe1a85ec53)
+        h ^= h >> np.uint64(33)
+    return h
+
+
+def test_colliding_hash_tags_stay_distinct():
+    # Strings whose 32-bit tags and first probe slot (64-slot table) agree: the
+    # second one finds the first's slot with a matching tag, so only the byte
+    # comparison keeps them apart.
+    say("[vocab] colliding tags")
+    n = 1 << 21
+    strings = [b"k%07d" % i for i in range(n)]
+    h = _np_hash(strings)
+    key = (h >> np.uint64(32)) << np.uint64(6) | (h & np.uint64(63))
+    order = np.argsort(key, kind="stable")
+    ks = key[order]
+    dup = np.nonzero(ks[1:] == ks[:-1])[0]
+    pairs = [(strings[order[i]], strings[order[i + 1]]) for i in dup[:8]]
+    assert pairs, "no colliding pair found"
+    for a, b in pairs:
+        S = [a, b, a, b, b, a]
+        O = [b, a, a, b, a, b]
+        P = [a, b, b, a, a, b]
+        ref = _compare([_column(S), _column(P), _column(O)], f"tags {a}/{b}", max_e=2, max_p=2)
+        assert ref[3] == 2 and ref[4] == 2
+
+
+@pytest.mark.parametrize("name", ["tiny_uniform", "uniform_1m", "powerlaw_20m"])
+def test_workloads_against_oracle(name):
+    w = synth.WORKLOADS[name]
+    say(f"[vocab] {w.describe()}")
+    S, P, O = synth.triples(w)
+    cols = synth.string_triples(S, P, O, w.num_entities, w.num_predicates)
+    _compare(cols, name, max_e=w.num_entities, max_p=w.num_predicates)
+
+
+def test_dense_workload_against_integer_ranks():
+    # 10M triples over 10k entities: every string recurs ~2000 times
+    w = synth.WORKLOADS["dense_10m"]
+    say(f"[vocab] {w.describe()}")
+    S, P, O = synth.triples(w)
+    cols = synth.string_triples(S, P, O, w.num_entities, w.num_predicates)
+    s, p, o, counts, flags = _run(cols, w.num_entities, w.num_predicates)
+    assert flags == 0
+    seq = np.empty(2 * len(S), np.int64)
+    seq[0::2], seq[1::2] = S, O
+    uniq, first = np.unique(seq, return_index=True)
+    rank = np.empty(w.num_entities, np.int64)
+    rank[uniq[np.argsort(first)]] = np.arange(uniq.size)
+    puniq, pfirst = np.unique(P, return_index=True)
+    prank = np.empty(w.num_predicates, np.int64)
+    prank[puniq[np.argsort(pfirst)]] = np.arange(puniq.size)
+    assert counts == [uniq.size, puniq.size]
+    assert np.array_equal(s, rank[S]) and np.array_equal(o, rank[O]) and np.array_equal(p, prank[P])
+
+
+def test_bound_exceeded_raises_capacity():
+    say("[vocab] capacity")
+    names = [b"e%d" % i for i in range(100)]
+    cols = [_column(names), _column([b"p"] * 100), _column(names[::-1])]
+    _, _, _, counts, flags = _run(cols, 100, 1)
+    assert flags == 0 and counts == [100, 1]
+    for max_e in (99, 40, 1):
+        _, _, _, counts, flags = _run(cols, max_e, 1)
+        assert flags & rd.RDF2V_STATUS_CAPACITY, max_e
+    _, _, _, _, flags = _run([cols[0], _column([b"p", b"q"] * 50), cols[2]], 100, 1)
+    assert flags == rd.RDF2V_STATUS_CAPACITY
+
+
+def test_bad_offsets_flagged():
+    say("[vocab] bad offsets")
+    chars, off = _column(["aa", "bb", "cc"])
+    for bad in ([0, 2, 1, 6], [0, 2, 4, 99], [-3, 2, 4, 6]):
+        cols = [(chars, np.array(bad, np.int64)), (chars, off), (chars, off)]
+        _, _, _, _, flags = _run(cols, 10, 10)
+        assert flags == rd.RDF2V_STATUS_BAD_LENGTH, bad
+
+
+def test_deterministic_across_calls_and_streams():
+    say("[vocab] determinism")
+    w = synth.WORKLOADS["uniform_1m"]
+    S, P, O = synth.triples(w)
+    cols = synth.string_triples(S, P, O, w.num_entities, w.num_predicates)
+    a = _run(cols, w.num_entities, w.num_predicates)
+    side = torch.cuda.Stream(device())
+    b = _run(cols, w.num_entities, w.num_predicates, stream=side)
+    for x, y in zip(a[:3], b[:3]):
+        assert np.array_equal(x, y)
+    assert a[3] == b[3]
+
+
+def test_string_pipeline_end_to_end():
+    # strings -> ids on the GPU -> CSR -> walks equals the oracle pipeline from the same strings
+    say("[vocab] end to end")
+    w = synth.WORKLOADS["tiny_uniform"]
+    S, P, O = synth.triples(w)
+    cols = synth.string_triples(S, P, O, w.num_entities, w.num_predicates)
+    st = new_status()
+    s, p, o, counts = rd.rdf2v_build_vocabulary(*[_dev_col(c) for c in cols], w.num_entities,
+                                                w.num_predicates, status=st)
+    V, Pn = [int(x) for x in counts.cpu()]
+    csr = rd.rdf2v_build_csr(s, p, o, V, Pn, status=st)
+    starts = rd.rdf2v_nonsink_starts(csr)
+    tok, ln = rd.rdf2v_random_walks(csr, starts, w.walks_per_node, w.depth, synth.WALK_SEED, status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    rs, rp_, ro, rV, rP = oracle.build_vocabulary(cols[0][0], cols[0][1], cols[1][0], cols[1][1], cols[2][0],
+                                                  cols[2][1])
+    assert (V, Pn) == (rV, rP)
+    row_ptr, edges = oracle.build_csr(rs, rp_, ro, rV, rP)
+    ref_starts = oracle.nonsink_starts(row_ptr, rV)
+    ref_t, ref_l = oracle.random_walks(row_ptr, edges, rV, rP, ref_starts, w.walks_per_node, w.depth,
+                                       synth.WALK_SEED)
+    assert np.array_equal(starts.cpu().numpy(), ref_starts)
+    assert np.array_equal(tok.cpu().numpy(), ref_t) and np.array_equal(ln.cpu().numpy(), ref_l)
