@@ -199,12 +199,14 @@ __global__ __launch_bounds__(kThreads) void init_kernel(Slot *__restrict__ table
   }
 }
 
+// Every used slot's minpos was lowered by the thread that claimed it, so it is
+// an occurrence in [0, n); the range check only guards the bitset.
 __global__ __launch_bounds__(kThreads) void mark_kernel(const Slot *__restrict__ table, int64_t capacity,
-                                                        unsigned long long *__restrict__ bits) {
+                                                        int64_t n, unsigned long long *__restrict__ bits) {
   const int64_t s = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   if (s >= capacity) return;
   const Slot t = table[s];
-  if (t.key == kEmpty) return;
+  if (t.key == kEmpty || t.minpos < 0 || t.minpos >= n) return;
   atomicOr(bits + (t.minpos >> 6), 1ull << (t.minpos & 63));
 }
 
@@ -260,13 +262,13 @@ __global__ __launch_bounds__(kThreads) void word_prefix_kernel(const uint64_t *_
   }
 }
 
-__global__ __launch_bounds__(kThreads) void slot_id_kernel(Slot *__restrict__ table, int64_t capacity,
+__global__ __launch_bounds__(kThreads) void slot_id_kernel(Slot *__restrict__ table, int64_t capacity, int64_t n,
                                                            const uint64_t *__restrict__ bits,
                                                            const int32_t *__restrict__ prefix) {
   const int64_t s = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   if (s >= capacity) return;
   const Slot t = table[s];
-  if (t.key == kEmpty) return;
+  if (t.key == kEmpty || t.minpos < 0 || t.minpos >= n) return;
   const int64_t w = t.minpos >> 6;
   const uint64_t below = (uint64_t(1) << (t.minpos & 63)) - 1;
   table[s].id = prefix[w] + __popcll(bits[w] & below);
@@ -325,7 +327,7 @@ rdf2v_status run_seq(const Seq &seq, const SeqPlan &p, int64_t max_distinct, cha
                                                                            status);
     RDF2V_LAUNCH_CHECK();
     mark_kernel<<<dim3(slot_blocks), dim3(kThreads), 0, stream>>>(
-        table, p.capacity, reinterpret_cast<unsigned long long *>(bits));
+        table, p.capacity, p.n, reinterpret_cast<unsigned long long *>(bits));
     RDF2V_LAUNCH_CHECK();
     popc_count_kernel<<<dim3(unsigned(p.blocks)), dim3(kThreads), 0, stream>>>(bits, p.words, partials);
     RDF2V_LAUNCH_CHECK();
@@ -336,7 +338,7 @@ rdf2v_status run_seq(const Seq &seq, const SeqPlan &p, int64_t max_distinct, cha
   if (p.n > 0) {
     word_prefix_kernel<<<dim3(unsigned(p.blocks)), dim3(kThreads), 0, stream>>>(bits, p.words, partials, prefix);
     RDF2V_LAUNCH_CHECK();
-    slot_id_kernel<<<dim3(slot_blocks), dim3(kThreads), 0, stream>>>(table, p.capacity, bits, prefix);
+    slot_id_kernel<<<dim3(slot_blocks), dim3(kThreads), 0, stream>>>(table, p.capacity, p.n, bits, prefix);
     RDF2V_LAUNCH_CHECK();
     assign_kernel<kPaired><<<dim3(occ_blocks), dim3(kThreads), 0, stream>>>(seq, p.n, table);
     RDF2V_LAUNCH_CHECK();
