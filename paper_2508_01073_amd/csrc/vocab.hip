@@ -3,23 +3,32 @@
 // dense ids, numbered by first appearance (entities over s_0, o_0, s_1, o_1,
 // ...; predicates over p_0, p_1, ...).
 //
-// Per sequence (entities, then predicates):
-//   1. insert_kernel:  one thread per occurrence q hashes its string and finds
-//                      or claims its slot in an open-addressing table (linear
-//                      probing, lock-free). A slot's 64-bit key is
-//                      (hash tag << 32 | representative occurrence), claimed
-//                      by one compare-and-swap; equal tags are always
-//                      confirmed byte by byte against the representative, so
-//                      hash collisions cannot merge two strings. The slot's
-//                      minpos becomes the smallest occurrence of its string
-//                      (read first, atomicMin only if smaller). The slot index
-//                      is parked in the id output.
-//   2. mark_kernel:    every used slot sets bit minpos of a bitset over the
-//                      occurrences: the first occurrences of all strings.
-//   3. popcount scan:  the rank of a first occurrence among all first
-//                      occurrences is its id (int32 prefix per 64-bit word).
-//   4. slot_id_kernel: the id of every used slot; assign_kernel replaces the
-//                      parked slot indices by ids.
+// Per sequence (entities, then predicates), with an open-addressing table of
+// 128-byte slots (linear probing, lock-free). A slot holds a 64-bit key
+// (20-bit hash tag, 12-bit length, representative occurrence) claimed by one
+// compare-and-swap, minpos (the smallest occurrence of its string) and an
+// inline copy of strings up to 98 bytes as 7-byte words, each with a
+// "written" byte on top, written by the claiming thread after its claim.
+//   1. insert_kernel (fast pass): a block stages the bytes of its strings in
+//      LDS with coalesced loads and hashes each string from there. For
+//      predicates, equal strings of the block are grouped first (exactly, in
+//      LDS) and only each group's first occurrence looks up the table. A
+//      lookup reads the key, minpos and the first inline word together, then
+//      the remaining words; equal tag and length plus equal inline words means
+//      the same string. A word not yet written leaves the occurrence to the
+//      general pass, as do strings that are not staged or too long to inline.
+//      No thread ever waits for another.
+//   2. insert_general_kernel: the deferred occurrences, one thread each, from
+//      global memory; equal tags are settled against the representative's
+//      bytes whenever the inline copy does not decide.
+//   Either pass lowers minpos (read first, atomicMin only if smaller) and
+//   parks the slot index in the id output.
+//   3. mark_kernel: every used slot sets bit minpos of a bitset over the
+//      occurrences: the first occurrences of all strings.
+//   4. popcount scan: the rank of a first occurrence among all first
+//      occurrences is its id (int32 prefix per 64-bit word).
+//   5. slot_id_kernel writes the id of every used slot to a compact array;
+//      assign_kernel replaces the parked slot indices by ids.
 // The table is sized to a power of two >= 2 * the caller's bound on distinct
 // strings, so probing stays short; the result does not depend on which thread
 // wins a slot, only on minpos, so it is deterministic.
@@ -36,12 +45,20 @@ constexpr int kThreads = 256;
 constexpr int kWordsPerThread = 16;
 constexpr int kWordTile = kThreads * kWordsPerThread;
 constexpr uint64_t kEmpty = ~uint64_t(0);
+constexpr int kInlineWords = 14;
+constexpr int kInlineBytes = 7 * kInlineWords;       // strings up to this long are copied into the slot
+constexpr uint64_t kWritten = uint64_t(1) << 56;      // top byte of an inline word once written
+constexpr uint64_t kLow56 = (uint64_t(1) << 56) - 1;
+constexpr int kStageWordsPerString = 16;              // LDS stage: 64 bytes per string of the block
+constexpr int64_t kLenField = 4095;                   // key length field (saturated)
 
-struct alignas(16) Slot {
-  uint64_t key;    // kEmpty, or (tag << 32) | representative occurrence
+struct alignas(128) Slot {
+  uint64_t key;    // kEmpty, or tag << 44 | min(len, 4095) << 32 | representative occurrence
   int32_t minpos;  // smallest occurrence of the slot's string
-  int32_t id;      // dense id, once ranked
+  int32_t spare;
+  uint64_t words[kInlineWords];  // inline copy: word i = bytes [7i, 7i + 7) | kWritten; 0 until written
 };
+static_assert(sizeof(Slot) == 128, "one slot per 128-byte line");
 
 struct StrCol {
   const uint8_t *chars;
@@ -77,36 +94,42 @@ __device__ __forceinline__ void string_range(const StrCol &c, int64_t row, int64
   len = b - a;
 }
 
-// Little-endian 4-byte word j of a column's chars (bytes past the end read 0).
+// Little-endian 4-byte word j of a column's chars (bytes outside it read 0).
 __device__ __forceinline__ uint32_t load_word(const StrCol &c, int64_t j) {
   const int64_t p = 4 * j;
-  if (p + 4 <= c.bytes) return reinterpret_cast<const uint32_t *>(c.chars)[j];
+  if (p >= 0 && p + 4 <= c.bytes) return reinterpret_cast<const uint32_t *>(c.chars)[j];
   uint32_t w = 0;
   for (int b = 0; b < 4; ++b)
-    if (p + b < c.bytes) w |= uint32_t(c.chars[p + b]) << (8 * b);
+    if (p + b >= 0 && p + b < c.bytes) w |= uint32_t(c.chars[p + b]) << (8 * b);
   return w;
 }
 
-// Consecutive 4-byte chunks of one string, read as aligned words and shifted;
-// the last chunk is zero-padded. The chunks depend on the bytes only, not on
-// where the string sits.
-struct ChunkReader {
-  const StrCol *c;
-  int64_t word;
-  int shift;
-  uint32_t lo;
-  __device__ __forceinline__ ChunkReader(const StrCol &col, int64_t start)
-      : c(&col), word(start >> 2), shift(int(start & 3) * 8) {
-    lo = load_word(col, word);
-  }
-  __device__ __forceinline__ uint32_t next(int64_t remaining) {
-    const uint32_t hi = load_word(*c, ++word);
-    uint32_t v = shift ? (lo >> shift) | (hi << (32 - shift)) : lo;
-    lo = hi;
-    if (remaining < 4) v &= (uint32_t(1) << (8 * remaining)) - 1;
-    return v;
-  }
-};
+__device__ __forceinline__ uint64_t low_bytes_mask(int64_t r) {  // the low min(r, 7) bytes
+  return r >= 7 ? kLow56 : (r <= 0 ? 0 : (uint64_t(1) << (8 * r)) - 1);
+}
+
+// Bytes [7i, 7i + 7) of a string as the low 56 bits of a word (zero past the
+// end). The LDS stage is padded with zero words, so its reads need no checks;
+// the global-memory form serves the general pass.
+__device__ __forceinline__ uint64_t word7_of(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t sh, int64_t r) {
+  const uint64_t lo = uint64_t(a0) | (uint64_t(a1) << 32);
+  // (a2 << 31) << (33 - sh) is a2 << (64 - sh), and 0 for sh == 0.
+  const uint64_t v = (lo >> sh) | ((uint64_t(a2) << 31) << (33 - sh));
+  return v & low_bytes_mask(r);
+}
+
+__device__ __forceinline__ uint64_t word7_lds(const uint32_t *lds, int32_t at, int64_t len, int i) {
+  const int32_t p = at + 7 * i;
+  const int32_t a = p >> 2;
+  return word7_of(lds[a], lds[a + 1], lds[a + 2], uint32_t(p & 3) * 8, len - 7 * int64_t(i));
+}
+
+__device__ __forceinline__ uint64_t word7_global(const StrCol *col, int64_t start, int64_t len, int64_t i) {
+  const int64_t p = start + 7 * i;
+  const int64_t a = p >> 2;
+  return word7_of(load_word(*col, a), load_word(*col, a + 1), load_word(*col, a + 2), uint32_t(p & 3) * 8,
+                  len - 7 * i);
+}
 
 __device__ __forceinline__ uint64_t fmix64(uint64_t h) {  // MurmurHash3 finaliser
   h ^= h >> 33;
@@ -117,74 +140,310 @@ __device__ __forceinline__ uint64_t fmix64(uint64_t h) {  // MurmurHash3 finalis
   return h;
 }
 
-__device__ __forceinline__ uint64_t string_hash(const StrCol &c, int64_t start, int64_t len) {
-  uint64_t h = 0x243f6a8885a308d3ull ^ (uint64_t(len) * 0x9e3779b97f4a7c15ull);
-  ChunkReader rd(c, start);
-  for (int64_t k = 0; k < len; k += 4) {
-    h = (h ^ rd.next(len - k)) * 0x100000001b3ull;
-    h ^= h >> 29;
-  }
-  return fmix64(h);
+__device__ __forceinline__ uint64_t hash_seed(int64_t len) {
+  return 0x243f6a8885a308d3ull ^ (uint64_t(len) * 0x9e3779b97f4a7c15ull);
+}
+__device__ __forceinline__ uint64_t hash_step(uint64_t h, uint64_t w) {
+  h = (h ^ w) * 0x100000001b3ull;
+  return h ^ (h >> 29);
 }
 
-__device__ __forceinline__ bool same_bytes(const StrCol &ca, int64_t a, const StrCol &cb, int64_t b,
-                                           int64_t len) {
-  ChunkReader ra(ca, a), rb(cb, b);
-  for (int64_t k = 0; k < len; k += 4)
-    if (ra.next(len - k) != rb.next(len - k)) return false;
-  return true;
+template <int kScope>
+__device__ __forceinline__ uint64_t load_u64(const uint64_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, kScope);
 }
 
-__device__ __forceinline__ uint64_t load_key(const Slot *s) {
-  return __hip_atomic_load(&s->key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+constexpr int kGroup = 1;           // inline words fetched together with the key
+constexpr int32_t kDeferred = -2;   // parked in the id output: left to the general pass
+
+// What one look at a slot returns: the key, minpos and the first inline words,
+// all loaded at once (one round trip; they share the slot's line).
+struct SlotView {
+  uint64_t key;
+  int32_t minpos;
+  uint64_t w[kGroup];
+};
+
+__device__ __forceinline__ SlotView view_slot(const Slot *sl, int nw) {
+  SlotView v;
+  v.key = load_u64<__HIP_MEMORY_SCOPE_AGENT>(&sl->key);
+  v.minpos = __hip_atomic_load(&sl->minpos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+  for (int i = 0; i < kGroup; ++i) v.w[i] = i < nw ? load_u64<__HIP_MEMORY_SCOPE_AGENT>(&sl->words[i]) : 0;
+  return v;
 }
 
-template <bool kPaired>
-__global__ __launch_bounds__(kThreads) void insert_kernel(Seq seq, int64_t n, Slot *__restrict__ table,
-                                                          int64_t mask, int32_t *status) {
-  const int64_t q = int64_t(blockIdx.x) * kThreads + threadIdx.x;
-  if (q >= n) return;
-  const int col = seq_col<kPaired>(q);
-  const StrCol &c = seq.col[col];
-  int bad = 0;
-  int64_t start, len;
-  string_range(c, seq_row<kPaired>(q), start, len, bad);
-  const uint64_t h = string_hash(c, start, len);
-  const uint32_t tag = uint32_t(h >> 32);
-  const uint64_t mine = (uint64_t(tag) << 32) | uint32_t(q);
+// The table slot of one string (staged in LDS, at most kInlineBytes long) for
+// occurrence q: found, or claimed (then its inline copy is written), with minpos
+// lowered to q where needed. Returns the slot, kDeferred when an equal tag and
+// length meet an inline copy not yet fully written (the general pass settles
+// it), or -1 when the table is full.
+__device__ __forceinline__ int32_t find_or_claim(Slot *__restrict__ table, int64_t mask, uint64_t h, int64_t q,
+                                                 const uint32_t *lds, int32_t at, int64_t len) {
+  const int nw = int((len + 6) / 7);
+  const uint64_t ident = ((h >> 44) << 12) | uint64_t(len);
+  const uint64_t mine = (ident << 32) | uint32_t(q);
   int64_t s = int64_t(h & uint64_t(mask));
-  int64_t found = -1;
   for (int64_t probe = 0; probe <= mask; ++probe, s = (s + 1) & mask) {
-    uint64_t k = load_key(table + s);
-    if (k == kEmpty) {
-      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long *>(&table[s].key),
+    Slot *sl = table + s;
+    SlotView v = view_slot(sl, nw);
+    if (v.key == kEmpty) {
+      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long *>(&sl->key),
                                       static_cast<unsigned long long>(kEmpty),
                                       static_cast<unsigned long long>(mine));
       if (prev == kEmpty) {
+        for (int i = 0; i < nw; ++i)
+          __hip_atomic_store(&sl->words[i], word7_lds(lds, at, len, i) | kWritten, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+        atomicMin(&sl->minpos, int32_t(q));
+        return int32_t(s);
+      }
+      v.key = prev;
+    }
+    if ((v.key >> 32) != ident) continue;
+    // Same tag and length: compare the inline copy (each word is written once,
+    // from 0, so a word is either not written yet or final).
+    bool unwritten = false, differ = false;
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      if (i < nw) {
+        if ((v.w[i] & ~kLow56) != kWritten)
+          unwritten = true;
+        else if (v.w[i] != (word7_lds(lds, at, len, i) | kWritten))
+          differ = true;
+      }
+    }
+#pragma unroll 1
+    for (int i = kGroup; i < nw; ++i) {
+      const uint64_t w = load_u64<__HIP_MEMORY_SCOPE_AGENT>(&sl->words[i]);
+      if ((w & ~kLow56) != kWritten)
+        unwritten = true;
+      else if (w != (word7_lds(lds, at, len, i) | kWritten))
+        differ = true;
+    }
+    if (differ) continue;  // a different string
+    if (unwritten) return kDeferred;
+    if (int32_t(q) < v.minpos) atomicMin(&sl->minpos, int32_t(q));
+    return int32_t(s);
+  }
+  return -1;
+}
+
+// Fast pass. A block stages its strings in LDS and hashes them from there.
+// With kGroupEqual, equal strings of the block are grouped first and only each
+// group's first occurrence, the leader, looks up the global table: a string
+// repeated within a block costs one lookup, so the slots of frequent strings
+// are not hammered by every occurrence. Occurrences whose strings are not
+// staged or too long for an inline copy, and lookups that were deferred, are
+// parked as kDeferred for the general pass.
+template <bool kPaired, int kBlock, bool kGroupEqual>
+__global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot *__restrict__ table,
+                                                        int64_t mask, int32_t *status) {
+  constexpr int kCols = kPaired ? 2 : 1;
+  constexpr int kWords = kBlock * kStageWordsPerString;
+  constexpr int kPerCol = kWords / kCols;  // includes kPad zero words
+  constexpr int kPad = 4;
+  constexpr int kLocal = 2 * kBlock;  // entries of the block's LDS table of distinct strings
+  __shared__ uint32_t stage[kWords];
+  __shared__ int64_t span[2][2];  // per column: off[first row], off[last row + 1]
+  // Grouping only (kGroupEqual):
+  __shared__ uint64_t blk_hash[kGroupEqual ? kBlock : 1];
+  __shared__ int32_t blk_at[kGroupEqual ? kBlock : 1];  // byte offset of the string in its column's stage
+  __shared__ int32_t blk_len[kGroupEqual ? kBlock : 1];
+  __shared__ int32_t loc_owner[kGroupEqual ? kLocal : 1];  // 1 + thread that claimed the entry, 0 if empty
+  __shared__ int32_t loc_min[kGroupEqual ? kLocal : 1];    // smallest thread of the entry's group: its leader
+  __shared__ int32_t loc_slot[kGroupEqual ? kLocal : 1];   // the leader's lookup result
+  const int tid = threadIdx.x;
+  const int64_t q0 = int64_t(blockIdx.x) * kBlock;
+  const int64_t q = q0 + tid;
+  const bool active = q < n;
+  const int col = seq_col<kPaired>(q);
+  const StrCol &c = seq.col[col];
+  if constexpr (kGroupEqual) {
+    for (int i = tid; i < kLocal; i += kBlock) {
+      loc_owner[i] = 0;
+      loc_min[i] = INT32_MAX;
+    }
+  }
+  int64_t start = 0, len = 0;
+  bool bad = false;
+  if (active) {
+    const int64_t row = seq_row<kPaired>(q);
+    const int64_t a = c.off[row], b = c.off[row + 1];
+    // The block's strings of one column are consecutive rows, so for valid
+    // offsets they span [off[first row], off[last row + 1]): the first and
+    // last thread of the column know those two offsets.
+    const int64_t q_last = min(q0 + kBlock, n) - 1;
+    if (q - q0 < kCols) span[col][0] = a;
+    if (q_last - q < kCols) span[col][1] = b;
+    bad = a < 0 || b < a || b > c.bytes;
+    start = a;
+    len = b - a;
+  }
+  __syncthreads();
+  // Stage that span in LDS when it fits.
+  int64_t base[kCols];
+  int32_t count[kCols];
+#pragma unroll
+  for (int cc = 0; cc < kCols; ++cc) {
+    const int64_t lo = span[cc][0], hi = span[cc][1];
+    const bool ok = lo >= 0 && lo <= hi && hi <= seq.col[cc].bytes;
+    base[cc] = ok ? (lo >> 2) : 0;
+    const int64_t words = ok ? ((hi + 3) >> 2) - base[cc] : -1;
+    count[cc] = (words >= 0 && words <= kPerCol - kPad) ? int32_t(words) : -1;
+    uint32_t *dst = stage + cc * kPerCol;
+    for (int32_t i = tid; i < count[cc]; i += kBlock) dst[i] = load_word(seq.col[cc], base[cc] + i);
+    if (count[cc] >= 0 && tid < kPad) dst[count[cc] + tid] = 0;
+  }
+  __syncthreads();
+
+  const int64_t my_base = (kPaired && col == 1) ? base[kCols - 1] : base[0];
+  const int32_t my_count = (kPaired && col == 1) ? count[kCols - 1] : count[0];
+  const bool fast = active && !bad && len <= kInlineBytes && my_count >= 0 && start >= 4 * my_base &&
+                    start + len <= 4 * (my_base + my_count);
+  const uint32_t *lds = stage + col * kPerCol;
+  const int32_t at = fast ? int32_t(start - 4 * my_base) : -1;
+  const int nw = fast ? int((len + 6) / 7) : 0;
+
+  // Hash over the string's 7-byte words, which also form the inline copy.
+  uint64_t h = hash_seed(len);
+#pragma unroll 1
+  for (int i = 0; i < nw; ++i) h = hash_step(h, word7_lds(lds, at, len, i));
+  h = fmix64(h);
+
+  int32_t *out = seq.out[col] + seq_row<kPaired>(q);
+  if constexpr (!kGroupEqual) {
+    if (fast) {
+      const int32_t r = find_or_claim(table, mask, h, q, lds, at, len);
+      if (r == -1 && status != nullptr) atomicOr(status, RDF2V_STATUS_CAPACITY);
+      *out = r;
+    } else if (active) {
+      *out = kDeferred;
+    }
+  } else {
+    blk_hash[tid] = h;
+    blk_at[tid] = at;
+    blk_len[tid] = int32_t(fast ? len : -1);
+    __syncthreads();
+    // Group equal strings of the block: an LDS table keyed by the hash, with
+    // equal hashes confirmed by length and bytes; the group's smallest thread
+    // (its first occurrence) is the leader.
+    int e = -1;
+    if (fast) {
+      e = int(h & uint64_t(kLocal - 1));
+      for (;;) {  // ends: the table has more entries than the block has threads
+        const int cur = atomicCAS(&loc_owner[e], 0, tid + 1);
+        bool same = cur == 0;
+        if (!same) {
+          const int o = cur - 1;
+          if (blk_hash[o] == h && blk_len[o] == int32_t(len)) {
+            const uint32_t *olds = stage + seq_col<kPaired>(q0 + o) * kPerCol;
+            const int32_t oat = blk_at[o];
+            same = true;
+            for (int i = 0; i < nw && same; ++i) same = word7_lds(olds, oat, len, i) == word7_lds(lds, at, len, i);
+          }
+        }
+        if (same) {
+          atomicMin(&loc_min[e], tid);
+          break;
+        }
+        e = (e + 1) & (kLocal - 1);
+      }
+    }
+    __syncthreads();
+    if (fast && loc_min[e] == tid) {
+      const int32_t r = find_or_claim(table, mask, h, q, lds, at, len);
+      loc_slot[e] = r;
+      if (r == -1 && status != nullptr) atomicOr(status, RDF2V_STATUS_CAPACITY);
+    }
+    __syncthreads();
+    if (active) *out = fast ? loc_slot[e] : kDeferred;
+  }
+}
+
+// Byte equality of two strings of the same length `len` in global memory.
+__device__ __forceinline__ bool same_string_global(const StrCol *ca, int64_t sa, const StrCol *cb, int64_t sb,
+                                                   int64_t len) {
+  const int64_t nw = (len + 6) / 7;
+  for (int64_t i = 0; i < nw; ++i)
+    if (word7_global(ca, sa, len, i) != word7_global(cb, sb, len, i)) return false;
+  return true;
+}
+
+// General pass over the deferred occurrences (bad offsets, strings outside
+// their block's stage, strings too long for an inline copy, compares left
+// undecided): the same hash and table, with strings read from global memory,
+// table loads at agent scope, and equal tags settled against the
+// representative's bytes whenever the inline copy does not decide.
+template <bool kPaired>
+__global__ __launch_bounds__(kThreads) void insert_general_kernel(Seq seq, int64_t n, Slot *__restrict__ table,
+                                                                  int64_t mask, int32_t *status) {
+  const int64_t q = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  if (q >= n) return;
+  const int col = seq_col<kPaired>(q);
+  int32_t *out = seq.out[col] + seq_row<kPaired>(q);
+  if (*out != kDeferred) return;
+  const StrCol *c = &seq.col[col];
+  int bad = 0;
+  int64_t start, len;
+  string_range(*c, seq_row<kPaired>(q), start, len, bad);
+  const int64_t words = (len + 6) / 7;
+  uint64_t h = hash_seed(len);
+  for (int64_t i = 0; i < words; ++i) h = hash_step(h, word7_global(c, start, len, i));
+  h = fmix64(h);
+  const uint64_t ident = ((h >> 44) << 12) | uint64_t(min(len, kLenField));
+  const uint64_t mine = (ident << 32) | uint32_t(q);
+  const int nw = len <= kInlineBytes ? int(words) : -1;  // -1: no inline copy
+  int64_t s = int64_t(h & uint64_t(mask));
+  int64_t found = -1;
+  for (int64_t probe = 0; probe <= mask; ++probe, s = (s + 1) & mask) {
+    Slot *sl = table + s;
+    uint64_t k = load_u64<__HIP_MEMORY_SCOPE_AGENT>(&sl->key);
+    if (k == kEmpty) {
+      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long *>(&sl->key),
+                                      static_cast<unsigned long long>(kEmpty),
+                                      static_cast<unsigned long long>(mine));
+      if (prev == kEmpty) {
+        for (int i = 0; i < nw; ++i)
+          __hip_atomic_store(&sl->words[i], word7_global(c, start, len, i) | kWritten, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
         found = s;
         break;
       }
       k = prev;
     }
-    if (uint32_t(k >> 32) != tag) continue;
-    const int64_t rep = int64_t(uint32_t(k));
-    const StrCol &rc = seq.col[seq_col<kPaired>(rep)];
-    int rbad = 0;
-    int64_t rstart, rlen;
-    string_range(rc, seq_row<kPaired>(rep), rstart, rlen, rbad);
-    if (rlen == len && same_bytes(c, start, rc, rstart, len)) {
+    if ((k >> 32) != ident) continue;
+    int same = -1;
+    if (nw >= 0) {
+      bool unwritten = false, differ = false;
+      for (int i = 0; i < nw && !differ; ++i) {
+        const uint64_t w = load_u64<__HIP_MEMORY_SCOPE_AGENT>(&sl->words[i]);
+        if ((w & ~kLow56) != kWritten)
+          unwritten = true;
+        else if (w != (word7_global(c, start, len, i) | kWritten))
+          differ = true;
+      }
+      same = differ ? 0 : (unwritten ? -1 : 1);
+    }
+    if (same < 0) {
+      const int64_t rep = int64_t(uint32_t(k));
+      const StrCol *rc = &seq.col[seq_col<kPaired>(rep)];
+      int rbad = 0;
+      int64_t rstart, rlen;
+      string_range(*rc, seq_row<kPaired>(rep), rstart, rlen, rbad);
+      same = (rlen == len && same_string_global(c, start, rc, rstart, len)) ? 1 : 0;
+    }
+    if (same == 1) {
       found = s;
       break;
     }
   }
-  int32_t *out = seq.out[col] + seq_row<kPaired>(q);
   if (found < 0) {
     *out = -1;
     if (status != nullptr) atomicOr(status, RDF2V_STATUS_CAPACITY);
   } else {
     int32_t *mp = &table[found].minpos;
-    if (int32_t(q) < __hip_atomic_load(mp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-      atomicMin(mp, int32_t(q));
+    if (int32_t(q) < __hip_atomic_load(mp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicMin(mp, int32_t(q));
     *out = int32_t(found);
   }
   if (bad && status != nullptr) atomicOr(status, RDF2V_STATUS_BAD_LENGTH);
@@ -194,7 +453,14 @@ __global__ __launch_bounds__(kThreads) void init_kernel(Slot *__restrict__ table
                                                         uint64_t *__restrict__ bits, int64_t words) {
   const int64_t stride = int64_t(gridDim.x) * kThreads;
   for (int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x; i < capacity || i < words; i += stride) {
-    if (i < capacity) table[i] = Slot{kEmpty, INT32_MAX, -1};
+    if (i < capacity) {
+      Slot &sl = table[i];
+      sl.key = kEmpty;
+      sl.minpos = INT32_MAX;
+      sl.spare = 0;
+#pragma unroll
+      for (int k = 0; k < kInlineWords; ++k) sl.words[k] = 0;
+    }
     if (i < words) bits[i] = 0;
   }
 }
@@ -205,9 +471,10 @@ __global__ __launch_bounds__(kThreads) void mark_kernel(const Slot *__restrict__
                                                         int64_t n, unsigned long long *__restrict__ bits) {
   const int64_t s = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   if (s >= capacity) return;
-  const Slot t = table[s];
-  if (t.key == kEmpty || t.minpos < 0 || t.minpos >= n) return;
-  atomicOr(bits + (t.minpos >> 6), 1ull << (t.minpos & 63));
+  const uint64_t key = table[s].key;
+  const int32_t m = table[s].minpos;
+  if (key == kEmpty || m < 0 || m >= n) return;
+  atomicOr(bits + (m >> 6), 1ull << (m & 63));
 }
 
 __global__ __launch_bounds__(kThreads) void popc_count_kernel(const uint64_t *__restrict__ bits, int64_t words,
@@ -262,35 +529,43 @@ __global__ __launch_bounds__(kThreads) void word_prefix_kernel(const uint64_t *_
   }
 }
 
-__global__ __launch_bounds__(kThreads) void slot_id_kernel(Slot *__restrict__ table, int64_t capacity, int64_t n,
-                                                           const uint64_t *__restrict__ bits,
-                                                           const int32_t *__restrict__ prefix) {
+__global__ __launch_bounds__(kThreads) void slot_id_kernel(const Slot *__restrict__ table, int64_t capacity,
+                                                           int64_t n, const uint64_t *__restrict__ bits,
+                                                           const int32_t *__restrict__ prefix,
+                                                           int32_t *__restrict__ ids) {
   const int64_t s = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   if (s >= capacity) return;
-  const Slot t = table[s];
-  if (t.key == kEmpty || t.minpos < 0 || t.minpos >= n) return;
-  const int64_t w = t.minpos >> 6;
-  const uint64_t below = (uint64_t(1) << (t.minpos & 63)) - 1;
-  table[s].id = prefix[w] + __popcll(bits[w] & below);
+  const uint64_t key = table[s].key;
+  const int32_t m = table[s].minpos;
+  if (key == kEmpty || m < 0 || m >= n) return;
+  const int64_t w = m >> 6;
+  const uint64_t below = (uint64_t(1) << (m & 63)) - 1;
+  ids[s] = prefix[w] + __popcll(bits[w] & below);
 }
 
 template <bool kPaired>
-__global__ __launch_bounds__(kThreads) void assign_kernel(Seq seq, int64_t n, const Slot *__restrict__ table) {
+__global__ __launch_bounds__(kThreads) void assign_kernel(Seq seq, int64_t n, const int32_t *__restrict__ ids) {
   const int64_t q = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   if (q >= n) return;
   int32_t *out = seq.out[seq_col<kPaired>(q)] + seq_row<kPaired>(q);
   const int32_t s = *out;
-  if (s >= 0) *out = table[s].id;
+  if (s >= 0) *out = ids[s];
 }
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Fast-pass block sizes: one-wave blocks for entities (no grouping, so no
+// reason to wait on other waves), 256 strings per block for predicates (more
+// repeats to group).
+constexpr int kFastBlockEntities = 64;
+constexpr int kFastBlockPredicates = 256;
 
 struct SeqPlan {
   int64_t n = 0;         // occurrences
   int64_t capacity = 0;  // table slots (power of two)
   int64_t words = 0;     // bitset words
   int64_t blocks = 0;    // popcount-scan blocks
-  size_t table_off = 0, bits_off = 0, prefix_off = 0, partials_off = 0, end = 0;
+  size_t table_off = 0, ids_off = 0, bits_off = 0, prefix_off = 0, partials_off = 0, end = 0;
 };
 
 SeqPlan plan_seq(int64_t n, int64_t max_distinct, size_t at) {
@@ -302,7 +577,8 @@ SeqPlan plan_seq(int64_t n, int64_t max_distinct, size_t at) {
   p.words = ceil_div(n, 64);
   p.blocks = ceil_div(p.words, kWordTile);
   p.table_off = at;
-  p.bits_off = p.table_off + align_up(size_t(p.capacity) * sizeof(Slot), 256);
+  p.ids_off = p.table_off + align_up(size_t(p.capacity) * sizeof(Slot), 256);
+  p.bits_off = p.ids_off + align_up(size_t(p.capacity) * 4, 256);
   p.prefix_off = p.bits_off + align_up(size_t(p.words) * 8, 256);
   p.partials_off = p.prefix_off + align_up(size_t(p.words) * 4, 256);
   p.end = p.partials_off + align_up(size_t(p.blocks + 1) * 8, 256);
@@ -313,6 +589,7 @@ template <bool kPaired>
 rdf2v_status run_seq(const Seq &seq, const SeqPlan &p, int64_t max_distinct, char *ws, int64_t *count_out,
                      int32_t *status, hipStream_t stream) {
   Slot *table = reinterpret_cast<Slot *>(ws + p.table_off);
+  int32_t *ids = reinterpret_cast<int32_t *>(ws + p.ids_off);
   uint64_t *bits = reinterpret_cast<uint64_t *>(ws + p.bits_off);
   int32_t *prefix = reinterpret_cast<int32_t *>(ws + p.prefix_off);
   int64_t *partials = reinterpret_cast<int64_t *>(ws + p.partials_off);
@@ -323,8 +600,14 @@ rdf2v_status run_seq(const Seq &seq, const SeqPlan &p, int64_t max_distinct, cha
   const unsigned occ_blocks = unsigned(ceil_div(p.n, kThreads));
   const unsigned slot_blocks = unsigned(ceil_div(p.capacity, kThreads));
   if (p.n > 0) {
-    insert_kernel<kPaired><<<dim3(occ_blocks), dim3(kThreads), 0, stream>>>(seq, p.n, table, p.capacity - 1,
-                                                                           status);
+    // Entities are mostly distinct within a block, predicates mostly repeated:
+    // group equal strings only where that saves lookups.
+    constexpr int kFastBlock = kPaired ? kFastBlockEntities : kFastBlockPredicates;
+    insert_kernel<kPaired, kFastBlock, !kPaired><<<dim3(unsigned(ceil_div(p.n, kFastBlock))), dim3(kFastBlock), 0,
+                                                   stream>>>(seq, p.n, table, p.capacity - 1, status);
+    RDF2V_LAUNCH_CHECK();
+    insert_general_kernel<kPaired><<<dim3(occ_blocks), dim3(kThreads), 0, stream>>>(seq, p.n, table,
+                                                                                   p.capacity - 1, status);
     RDF2V_LAUNCH_CHECK();
     mark_kernel<<<dim3(slot_blocks), dim3(kThreads), 0, stream>>>(
         table, p.capacity, p.n, reinterpret_cast<unsigned long long *>(bits));
@@ -338,9 +621,9 @@ rdf2v_status run_seq(const Seq &seq, const SeqPlan &p, int64_t max_distinct, cha
   if (p.n > 0) {
     word_prefix_kernel<<<dim3(unsigned(p.blocks)), dim3(kThreads), 0, stream>>>(bits, p.words, partials, prefix);
     RDF2V_LAUNCH_CHECK();
-    slot_id_kernel<<<dim3(slot_blocks), dim3(kThreads), 0, stream>>>(table, p.capacity, p.n, bits, prefix);
+    slot_id_kernel<<<dim3(slot_blocks), dim3(kThreads), 0, stream>>>(table, p.capacity, p.n, bits, prefix, ids);
     RDF2V_LAUNCH_CHECK();
-    assign_kernel<kPaired><<<dim3(occ_blocks), dim3(kThreads), 0, stream>>>(seq, p.n, table);
+    assign_kernel<kPaired><<<dim3(occ_blocks), dim3(kThreads), 0, stream>>>(seq, p.n, ids);
     RDF2V_LAUNCH_CHECK();
   }
   return RDF2V_OK;

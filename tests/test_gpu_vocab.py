@@ -95,19 +95,38 @@ def test_near_duplicates_every_alignment(seed):
     _compare(cols, "exact bounds", max_e=ref[3], max_p=ref[4])
 
 
+def test_inline_copy_length_boundary():
+    # Strings of 96..100 bytes differing only in their last byte: up to 98 bytes
+    # they are compared against the slot's inline copy, beyond it against the
+    # representative's bytes.
+    say("[vocab] inline length boundary")
+    stem = bytes(range(7, 107))
+    pool = [stem[:L - 1] + bytes([b]) for L in range(96, 101) for b in range(4)]
+    rng = np.random.default_rng(5)
+    T = 500
+    for lead in range(4):
+        cols = [_column([pool[i] for i in rng.integers(0, len(pool), T)], lead=lead) for _ in range(3)]
+        ref = _compare(cols, f"boundary lead={lead}", max_e=len(pool), max_p=len(pool))
+        assert ref[3] == len(pool)
+
+
 def _np_hash(strings):
     """The library's 64-bit string hash, restated in numpy for equal-length strings
-    (used only to construct strings whose hash tags collide)."""
+    (used only to construct strings whose hash tags collide): the string as
+    little-endian 7-byte words, zero-padded, folded in after a length-seeded start,
+    then MurmurHash3's 64-bit finaliser."""
     M = (1 << 64) - 1
     n = len(strings[0])
     a = np.frombuffer(b"".join(strings), np.uint8).reshape(len(strings), n)
-    pad = (-n) % 4
-    a = np.concatenate([a, np.zeros((len(strings), pad), np.uint8)], axis=1)
-    chunks = a.view("<u4").astype(np.uint64)
+    nw = (n + 6) // 7
+    a = np.concatenate([a, np.zeros((len(strings), 7 * nw - n), np.uint8)], axis=1).reshape(len(strings), nw, 7)
+    words = np.zeros((len(strings), nw), np.uint64)
+    for b in range(7):
+        words |= a[:, :, b].astype(np.uint64) << np.uint64(8 * b)
     with np.errstate(over="ignore"):
         h = np.full(len(strings), np.uint64(0x243f6a8885a308d3 ^ ((n * 0x9e3779b97f4a7c15) & M)))
-        for k in range(chunks.shape[1]):
-            h = (h ^ chunks[:, k]) * np.uint64(0x100000001b3)
+        for k in range(nw):
+            h = (h ^ words[:, k]) * np.uint64(0x100000001b3)
             h ^= h >> np.uint64(29)
         h ^= h >> np.uint64(33)
         h *= np.uint64(0xff51afd7ed558ccd)
@@ -117,25 +136,28 @@ def _np_hash(strings):
     return h
 
 
-def test_colliding_hash_tags_stay_distinct():
-    # Strings whose 32-bit tags and first probe slot (64-slot table) agree: the
-    # second one finds the first's slot with a matching tag, so only the byte
-    # comparison keeps them apart.
-    say("[vocab] colliding tags")
-    n = 1 << 21
-    strings = [b"k%07d" % i for i in range(n)]
+@pytest.mark.parametrize("stem", [b"k", b"long-" * 20])
+def test_colliding_hash_tags_stay_distinct(stem):
+    # Equal-length strings whose 20-bit hash tags and first probe slot (64-slot
+    # table) agree: the second finds the first's slot with a matching tag and
+    # length, so only the byte comparison keeps them apart -- against the inline
+    # copy for short strings, against the representative's bytes for strings too
+    # long to be copied into the slot (105 bytes).
+    say(f"[vocab] colliding tags, {len(stem) + 5}-byte strings")
+    n = 1 << 16
+    strings = [stem + b"%05d" % i for i in range(n)]
     h = _np_hash(strings)
-    key = (h >> np.uint64(32)) << np.uint64(6) | (h & np.uint64(63))
+    key = (h >> np.uint64(44)) << np.uint64(6) | (h & np.uint64(63))
     order = np.argsort(key, kind="stable")
     ks = key[order]
     dup = np.nonzero(ks[1:] == ks[:-1])[0]
     pairs = [(strings[order[i]], strings[order[i + 1]]) for i in dup[:8]]
-    assert pairs, "no colliding pair found"
+    assert len(pairs) >= 4, "too few colliding pairs found"
     for a, b in pairs:
         S = [a, b, a, b, b, a]
         O = [b, a, a, b, a, b]
         P = [a, b, b, a, a, b]
-        ref = _compare([_column(S), _column(P), _column(O)], f"tags {a}/{b}", max_e=2, max_p=2)
+        ref = _compare([_column(S), _column(P), _column(O)], f"tags {a[-5:]}/{b[-5:]}", max_e=2, max_p=2)
         assert ref[3] == 2 and ref[4] == 2
 
 
