@@ -323,7 +323,7 @@ size_t rdf2v_build_vocabulary_workspace_size(int64_t num_triples, int64_t max_en
  *   num_triples     0 .. RDF2V_VOCAB_MAX_TRIPLES.
  *   max_entities,   caller's upper bounds on the distinct entity and predicate
  *   max_predicates  strings, 1 .. RDF2V_VOCAB_MAX_DISTINCT; they size the hash
- *                   tables (2 to 4 x the bound, 16 B a slot). More distinct
+ *                   tables (2 to 4 slots of 132 B per bounded string). More distinct
  *                   strings than a bound raise RDF2V_STATUS_CAPACITY.
  *   subj_ids, pred_ids, obj_ids  [num_triples] int32 outputs (device).
  *   counts_out      [2] int64 (device): distinct entities, distinct predicates.

@@ -255,10 +255,10 @@ def test_vocabulary_validation(lib):
     assert call(ws=None) == pkg.RDF2V_ERR_WORKSPACE
     assert call(nbytes=need - 1) == pkg.RDF2V_ERR_WORKSPACE
     assert call(ws=ctypes.c_void_p((1 << 41) + 16)) == pkg.RDF2V_ERR_WORKSPACE
-    # the tables are sized from the bounds: 2 to 4 slots of 16 B per distinct string
+    # the tables are sized from the bounds: 2 to 4 slots (128 B + a 4-byte id) per bounded string
     small = pkg.rdf2v_build_vocabulary_workspace_size(10**6, 1000, 10)
     big = pkg.rdf2v_build_vocabulary_workspace_size(10**6, 10**6, 10)
-    assert 2 * 16 * (10**6 - 1000) <= big - small <= 4 * 16 * 10**6
+    assert 2 * 132 * (10**6 - 1000) <= big - small <= 4 * 132 * 10**6
     assert pkg.rdf2v_build_vocabulary_workspace_size(-1, 1, 1) == 0
 
 
