@@ -93,12 +93,11 @@ def cpu_baseline(w, s, p, o, target_seconds: float):
     rate = probe / max(time.perf_counter() - t0, 1e-9)
     sample = int(min(num_walks, max(probe, rate * target_seconds)))
     t0 = time.perf_counter()
-    _, ln = oracle.random_walks(rp, ed, V, P, starts, w.walks_per_node, w.depth, 42, 0, sample)
+    tokens = oracle_walk_tokens(oracle, rp, ed, V, P, starts, w, 0, sample)
     t_walk = time.perf_counter() - t0
-    tokens = int(ln.astype(np.int64).sum())
     # the CSR build is charged in proportion to the sampled share of the walks
     t_step_share = t_walk + t_build * sample / num_walks
-    return {
+    out = {
         "value": tokens / t_step_share,
         "unit": "tokens/s",
         "cores": 1,
@@ -106,7 +105,50 @@ def cpu_baseline(w, s, p, o, target_seconds: float):
         "sample": (f"oracle CSR build over all {w.num_triples:,} triples ({t_build:.2f} s, charged "
                    f"pro rata) + the first {sample:,} of {num_walks:,} walks ({t_walk:.2f} s), "
                    f"single thread on {os.cpu_count()} visible host cores"),
+        "cpu_model": cpu_model(),
     }
+    out["all_cores"] = cpu_baseline_threads(oracle, rp, ed, V, P, starts, w, rate, target_seconds / 2)
+    return out
+
+
+def oracle_walk_tokens(oracle, rp, ed, V, P, starts, w, lo: int, hi: int, piece: int = 500_000) -> int:
+    """Valid tokens of the oracle's walks [lo, hi), produced piece by piece to bound host memory."""
+    import numpy as np
+    toks = 0
+    for b in range(lo, hi, piece):
+        _, ln = oracle.random_walks(rp, ed, V, P, starts, w.walks_per_node, w.depth, 42, b, min(piece, hi - b))
+        toks += int(ln.astype(np.int64).sum())
+    return toks
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline_threads(oracle, rp, ed, V, P, starts, w, rate_1t: float, seconds: float):
+    """The same oracle function in N threads over disjoint walk ranges (each ctypes call runs
+    without the GIL), N = the host threads this process may use (at most 16); walks only,
+    about `seconds` of wall time."""
+    import concurrent.futures
+    n = max(1, min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()))
+    num_walks = len(starts) * w.walks_per_node
+    per_thread = int(min(num_walks // n, max(1000, rate_1t * seconds)))
+
+    def run(i):
+        return oracle_walk_tokens(oracle, rp, ed, V, P, starts, w, i * per_thread, (i + 1) * per_thread)
+
+    t0 = time.perf_counter()
+    with concurrent.futures.ThreadPoolExecutor(max_workers=n) as pool:
+        tokens = sum(pool.map(run, range(n)))
+    elapsed = time.perf_counter() - t0
+    return {"value": tokens / elapsed, "unit": "tokens/s", "threads": n,
+            "sample": f"walks [0, {n * per_thread:,}) in {n} disjoint ranges, {elapsed:.2f} s wall (walks only)"}
 
 
 def time_pairs(rd, torch, tokens, lens, n_walks, batch_cap, width, window, pair_batch, stream, ev):
