@@ -106,22 +106,24 @@ __global__ __launch_bounds__(kThreads) void pair_offsets_kernel(const int32_t *_
   }
 }
 
-// One thread per (walk, center); walks_per_block = kThreads / width walks per
-// block, whose pairs form one contiguous output range. When that range fits in
-// LDS (kStagePairs), the threads place their pairs there and the block streams
-// the range out with consecutive, non-temporal 8-byte stores; otherwise each
-// thread writes its pairs directly.
-constexpr int kStagePairs = 4096;
+// One thread per (walk, center); walks_per_block = kBlock / width walks per
+// block, whose rows are contiguous in the input and whose pairs form one
+// contiguous output range. When that range fits in LDS (kStagePairs), the block
+// first copies its rows to LDS with one coalesced load, the threads place their
+// pairs in LDS, and the block streams the range out with consecutive,
+// non-temporal 16-byte stores; otherwise each thread reads its row from global
+// memory and writes its pairs directly. kStagePairs is the LDS stage, in pairs.
 
-template <bool kStage>
-__global__ __launch_bounds__(kThreads) void pair_emit_kernel(const int32_t *__restrict__ tokens,
+template <bool kStage, int kBlock, int kStagePairs>
+__global__ __launch_bounds__(kBlock) void pair_emit_kernel(const int32_t *__restrict__ tokens,
                                                              const int32_t *__restrict__ len, int64_t n,
                                                              int32_t width, int32_t window,
                                                              const int64_t *__restrict__ offsets,
                                                              int2 *__restrict__ pairs, int64_t capacity,
                                                              int32_t *status) {
   __shared__ int2 stage[kStage ? kStagePairs : 1];
-  const int walks_per_block = kThreads / width;
+  __shared__ int32_t rows[kStage ? kBlock : 1];  // the block's walk rows, walks_per_block * width tokens
+  const int walks_per_block = kBlock / width;
   const int t = threadIdx.x;
   const int64_t r0 = int64_t(blockIdx.x) * walks_per_block;
   const int64_t r_end = min(n, r0 + walks_per_block);
@@ -136,9 +138,25 @@ __global__ __launch_bounds__(kThreads) void pair_emit_kernel(const int32_t *__re
     L = clamped_len(len, r, width, bad);
     first = offsets[r] + capped_prefix(i, w) + capped_prefix(L, w) - capped_prefix(L - i, w);
   }
+  // The block's pairs end where the next block's begin: the offset of walk
+  // r_end, or the pair count of the last walk added to its offset.
+  __shared__ int64_t block_end;
+  if (kStage) {
+    const int64_t span = (r_end - r0) * width;  // <= kBlock
+    if (t < span) rows[t] = tokens[r0 * width + t];
+    if (t == 0) {
+      if (r_end < n) {
+        block_end = offsets[r_end];
+      } else {
+        int b2 = 0;
+        block_end = offsets[n - 1] + walk_pairs(clamped_len(len, n - 1, width, b2), w);
+      }
+    }
+    __syncthreads();
+  }
   bool full = false;
   if (active && i < L) {
-    const int32_t *row = tokens + r * width;
+    const int32_t *row = kStage ? rows + (t / width) * width : tokens + r * width;
     const int32_t center = row[i];
     const int64_t j0 = max(int64_t(0), i - w), j1 = min(L - 1, i + w);
     int64_t k = first;
@@ -157,16 +175,6 @@ __global__ __launch_bounds__(kThreads) void pair_emit_kernel(const int32_t *__re
   }
   if (kStage) {
     __syncthreads();
-    // The block's pairs end where the next block's begin: the offset of walk
-    // r_end, or the pair count of the last walk added to its offset.
-    __shared__ int64_t block_end;
-    if (t == 0) {
-      int b2 = 0;
-      const int64_t last = r_end - 1;
-      const int64_t Ll = clamped_len(len, last, width, b2);
-      block_end = offsets[last] + walk_pairs(Ll, w);
-    }
-    __syncthreads();
     const int64_t cnt = block_end - block_first;
     if (block_end > capacity) full = true;
     const int64_t lim = min(cnt, capacity - block_first);  // pairs of this block that fit
@@ -177,7 +185,7 @@ __global__ __launch_bounds__(kThreads) void pair_emit_kernel(const int32_t *__re
       __builtin_nontemporal_store(v2i32{stage[0].x, stage[0].y}, reinterpret_cast<v2i32 *>(pairs + block_first));
     const int64_t body = lim > head ? (lim - head) >> 1 : 0;
     v4i32 *dst = reinterpret_cast<v4i32 *>(pairs + block_first + head);
-    for (int64_t q = t; q < body; q += kThreads) {
+    for (int64_t q = t; q < body; q += kBlock) {
       const int2 a = stage[head + 2 * q], b = stage[head + 2 * q + 1];
       __builtin_nontemporal_store(v4i32{a.x, a.y, b.x, b.y}, dst + q);
     }
@@ -225,17 +233,23 @@ rdf2v_status launch_skipgram_pairs(const int32_t *tokens, const int32_t *len, in
                                                                         partials, offsets);
   RDF2V_LAUNCH_CHECK();
   if (capacity > 0) {
-    const int walks_per_block = kThreads / width;
-    const int64_t blocks = ceil_div(num_walks, walks_per_block);
-    if (blocks >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
     int2 *out = reinterpret_cast<int2 *>(pairs_out);
-    if (max_walk_pairs(width, window) * walks_per_block <= kStagePairs)
-      pair_emit_kernel<true><<<dim3(unsigned(blocks)), dim3(kThreads), 0, stream>>>(
-          tokens, len, num_walks, width, window, offsets, out, capacity, status_dev);
-    else
-      pair_emit_kernel<false><<<dim3(unsigned(blocks)), dim3(kThreads), 0, stream>>>(
-          tokens, len, num_walks, width, window, offsets, out, capacity, status_dev);
-    RDF2V_LAUNCH_CHECK();
+    // The largest block whose pairs still fit the LDS stage: more walks per
+    // block for short windows, so that each block streams a longer range.
+    const int64_t per_walk = max_walk_pairs(width, window);
+    auto fits = [&](int block, int stage) { return width <= block && per_walk * (block / width) <= stage; };
+    auto launch = [&](auto kernel, int block) -> rdf2v_status {
+      const int64_t blocks = ceil_div(num_walks, block / width);
+      if (blocks >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
+      kernel<<<dim3(unsigned(blocks)), dim3(block), 0, stream>>>(tokens, len, num_walks, width, window, offsets,
+                                                                 out, capacity, status_dev);
+      RDF2V_LAUNCH_CHECK();
+      return RDF2V_OK;
+    };
+    if (fits(1024, 4096)) return launch(pair_emit_kernel<true, 1024, 4096>, 1024);
+    if (fits(512, 5120)) return launch(pair_emit_kernel<true, 512, 5120>, 512);
+    if (fits(kThreads, 4096)) return launch(pair_emit_kernel<true, kThreads, 4096>, kThreads);
+    return launch(pair_emit_kernel<false, kThreads, 1>, kThreads);
   }
   return RDF2V_OK;
 }
