@@ -2,15 +2,20 @@
 // free"): within each group of consecutive rows (the walks of one start
 // entity) keep the first occurrence of every distinct walk, in row order.
 //
-//   1. row_hash_kernel:  a 64-bit hash of (len, valid tokens) per row;
-//   2. keep_kernel:      row r is kept unless an earlier row of its group has
-//                        the same hash, the same length and the same tokens
-//                        (equal hashes are always confirmed token by token, so
-//                        collisions cannot drop a walk);
-//   3. count / scan / compact: an order-preserving stream compaction of the
-//                        kept rows (int64 offsets).
-// Integer streaming work; the group scan of step 2 reads hashes that are
-// L1/L2-resident because the rows of a group are adjacent.
+// Main path (groups of at most 1024 rows whose block of rows fits the LDS
+// stage): a block owns whole groups.
+//   1. group_keep_kernel: the block copies its rows to LDS (batched coalesced
+//      loads), hashes every row there (64-bit FNV-1a over length and valid
+//      tokens), and keeps a row unless an earlier row of its group has the same
+//      hash, length and tokens (equal hashes are always confirmed token by
+//      token, so collisions cannot drop a walk). Keep flags go to global
+//      memory, the block's kept count to a partial sum.
+//   2. keep_partials_kernel: exclusive scan of the block counts.
+//   3. group_compact_kernel: the block stages its rows again, scans its keep
+//      flags and writes its kept rows as one contiguous range.
+// Other shapes use the general path: a hash per row, a group scan over the
+// hashes in global memory, and the same scan and order-preserving compaction
+// over tiles of rows. Integer streaming work.
 
 #include "common.hpp"
 #include "launch.hpp"
@@ -103,16 +108,28 @@ __global__ __launch_bounds__(kThreads) void keep_count_kernel(const int32_t *__r
   if (threadIdx.x == 0) partials[blockIdx.x] = total;
 }
 
+// One block: exclusive scan of the nb block counts in place, kItems consecutive
+// counts per thread per round; the total goes to partials[nb] and *total_out.
 __global__ __launch_bounds__(kThreads) void keep_partials_kernel(int64_t *partials, int64_t nb,
                                                                  int64_t *total_out) {
   __shared__ int64_t scratch[kThreads / kWave];
   int64_t carry = 0;
-  for (int64_t base = 0; base < nb; base += kThreads) {
-    const int64_t idx = base + threadIdx.x;
-    const int64_t x = idx < nb ? partials[idx] : 0;
+  for (int64_t base = 0; base < nb; base += kTile) {
+    const int64_t first = base + int64_t(threadIdx.x) * kItems;
+    int64_t v[kItems];
+    int64_t s = 0;
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      v[i] = first + i < nb ? partials[first + i] : 0;
+      s += v[i];
+    }
     int64_t tot;
-    const int64_t ex = block_exclusive_scan<kThreads, int64_t>(x, scratch, tot);
-    if (idx < nb) partials[idx] = carry + ex;
+    int64_t ex = carry + block_exclusive_scan<kThreads, int64_t>(s, scratch, tot);
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      if (first + i < nb) partials[first + i] = ex;
+      ex += v[i];
+    }
     carry += tot;
   }
   if (threadIdx.x == 0) {
@@ -162,6 +179,110 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const int32_t *__rest
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// ---------------------------------------------------------------------------
+// Main path: blocks of whole groups.
+// ---------------------------------------------------------------------------
+
+constexpr int kGroupStageInts = 12288;  // at most 48 KiB of rows per block (dynamic LDS, sized per launch)
+constexpr int kBatch = 8;               // loads in flight per thread while staging
+
+// Copies `count` ints from global memory to LDS, kBatch independent loads per
+// thread at a time (NT threads).
+template <int NT>
+__device__ __forceinline__ void stage_ints(int32_t *__restrict__ dst, const int32_t *__restrict__ src,
+                                           int32_t count) {
+  for (int32_t base = 0; base < count; base += kBatch * NT) {
+    int32_t v[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int32_t q = base + k * NT + int32_t(threadIdx.x);
+      v[k] = q < count ? src[q] : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int32_t q = base + k * NT + int32_t(threadIdx.x);
+      if (q < count) dst[q] = v[k];
+    }
+  }
+}
+
+// Rows [b * rows_per_block, ...) of block b, rows_per_block = (NT / group) * group.
+template <int NT>
+__global__ __launch_bounds__(NT) void group_keep_kernel(const int32_t *__restrict__ tokens,
+                                                              const int32_t *__restrict__ len, int64_t n,
+                                                              int32_t width, int32_t group, int32_t rows_per_block,
+                                                              uint8_t *__restrict__ keep,
+                                                              int64_t *__restrict__ partials, int32_t *status) {
+  extern __shared__ int32_t tile[];  // rows_per_block * width ints
+  __shared__ uint64_t hashes[NT];
+  __shared__ int32_t lens[NT];
+  __shared__ int64_t scratch[NT / kWave];
+  const int64_t r0 = int64_t(blockIdx.x) * rows_per_block;
+  const int32_t rows = int32_t(min(int64_t(rows_per_block), n - r0));
+  stage_ints<NT>(tile, tokens + r0 * width, rows * width);
+  __syncthreads();
+  const int t = threadIdx.x;
+  int bad = 0;
+  int32_t L = 0;
+  if (t < rows) {
+    L = clamp_len(len[r0 + t], width, bad);
+    hashes[t] = row_hash(tile + t * width, L);
+    lens[t] = L;
+  }
+  __syncthreads();
+  int32_t k = 0;
+  if (t < rows) {
+    const uint64_t h = hashes[t];
+    const int32_t *row = tile + t * width;
+    bool dup = false;
+    for (int32_t q = t / group * group; q < t && !dup; ++q) {
+      if (hashes[q] != h || lens[q] != L) continue;
+      const int32_t *other = tile + q * width;
+      bool same = true;
+      for (int32_t j = 0; j < L && same; ++j) same = other[j] == row[j];
+      dup = same;
+    }
+    k = dup ? 0 : 1;
+    keep[r0 + t] = uint8_t(k);
+  }
+  const int64_t total = block_sum<NT, int64_t>(k, scratch);
+  if (t == 0) partials[blockIdx.x] = total;
+  if (bad && status != nullptr) atomicOr(status, RDF2V_STATUS_BAD_LENGTH);
+}
+
+template <int NT>
+__global__ __launch_bounds__(NT) void group_compact_kernel(const int32_t *__restrict__ tokens,
+                                                                 const int32_t *__restrict__ len, int64_t n,
+                                                                 int32_t width, int32_t rows_per_block,
+                                                                 const uint8_t *__restrict__ keep,
+                                                                 const int64_t *__restrict__ partials,
+                                                                 int32_t *__restrict__ tokens_out,
+                                                                 int32_t *__restrict__ len_out) {
+  extern __shared__ int32_t tile[];  // rows_per_block * width ints
+  __shared__ int32_t kept_rows[NT];
+  __shared__ int64_t scratch[NT / kWave];
+  const int64_t r0 = int64_t(blockIdx.x) * rows_per_block;
+  const int32_t rows = int32_t(min(int64_t(rows_per_block), n - r0));
+  stage_ints<NT>(tile, tokens + r0 * width, rows * width);
+  const int t = threadIdx.x;
+  const int64_t k = t < rows ? keep[r0 + t] : 0;
+  int64_t tot;
+  const int64_t ex = block_exclusive_scan<NT, int64_t>(k, scratch, tot);  // also orders the stage
+  const int64_t out0 = partials[blockIdx.x];
+  if (k) {
+    kept_rows[ex] = t;
+    len_out[out0 + ex] = len[r0 + t];
+  }
+  __syncthreads();
+  // The block's kept rows form one contiguous output range.
+  const int32_t span = int32_t(tot) * width;
+  int32_t *dst = tokens_out + out0 * width;
+  for (int32_t q = t; q < span; q += NT) {
+    const int32_t kr = q / width;
+    dst[q] = tile[kept_rows[kr] * width + (q - kr * width)];
+  }
+}
+
 }  // namespace
 
 size_t unique_walks_workspace_bytes(int64_t num_walks) {
@@ -175,6 +296,36 @@ rdf2v_status launch_unique_walks(const int32_t *tokens, const int32_t *len, int6
                                  int64_t *count_out, void *workspace, int32_t *status_dev,
                                  hipStream_t stream) {
   char *ws = static_cast<char *>(workspace);
+  // Main path: blocks of whole groups (256 threads, or 1024 for groups of up
+  // to 1024 rows), when the block's rows fit the LDS stage. Workspace: the
+  // block partials where the general path keeps its hashes (8 B per row >=
+  // 8 B per block + 1), the keep flags after them.
+  int64_t *block_counts = reinterpret_cast<int64_t *>(ws);
+  uint8_t *keep_flags = reinterpret_cast<uint8_t *>(ws + align_up(size_t(num_walks) * 8, 256));
+  auto main_path = [&](auto keep_kernel, auto compact_kernel, int nt) -> rdf2v_status {
+    const int32_t rows_per_block = (nt / group) * group;
+    const size_t tile_bytes = size_t(rows_per_block) * width * sizeof(int32_t);
+    const int64_t nb = ceil_div(num_walks, rows_per_block);
+    if (nb >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
+    if (nb > 0) {
+      keep_kernel<<<dim3(unsigned(nb)), dim3(nt), tile_bytes, stream>>>(tokens, len, num_walks, width, group,
+                                                                        rows_per_block, keep_flags, block_counts,
+                                                                        status_dev);
+      RDF2V_LAUNCH_CHECK();
+    }
+    keep_partials_kernel<<<dim3(1), dim3(kThreads), 0, stream>>>(block_counts, nb, count_out);
+    RDF2V_LAUNCH_CHECK();
+    if (nb > 0) {
+      compact_kernel<<<dim3(unsigned(nb)), dim3(nt), tile_bytes, stream>>>(tokens, len, num_walks, width,
+                                                                           rows_per_block, keep_flags, block_counts,
+                                                                           tokens_out, len_out);
+      RDF2V_LAUNCH_CHECK();
+    }
+    return RDF2V_OK;
+  };
+  auto fits = [&](int nt) { return group <= nt && int64_t(nt / group) * group * width <= kGroupStageInts; };
+  if (fits(kThreads)) return main_path(group_keep_kernel<kThreads>, group_compact_kernel<kThreads>, kThreads);
+  if (fits(1024)) return main_path(group_keep_kernel<1024>, group_compact_kernel<1024>, 1024);
   uint64_t *hash = reinterpret_cast<uint64_t *>(ws);
   int32_t *keep = reinterpret_cast<int32_t *>(ws + align_up(size_t(num_walks) * 8, 256));
   int64_t *partials = reinterpret_cast<int64_t *>(ws + align_up(size_t(num_walks) * 8, 256) +

@@ -99,6 +99,23 @@ def test_unique_walks_random_rows_and_ragged_groups():
         assert_rows_equal(got_t, got_l, ref_t, ref_l, f"group {group}")
 
 
+@pytest.mark.parametrize("width,group", [(9, 1), (17, 50), (33, 64), (33, 300), (9, 1000), (65, 10), (129, 3),
+                                         (5, 1024), (5, 1025)])
+def test_unique_walks_row_widths_and_group_sizes(width, group):
+    # blocks of whole groups (256 or 1024 threads) where the rows fit the LDS
+    # stage, the general path otherwise; both against the oracle
+    say(f"[unique] width {width} group {group}")
+    rng = np.random.default_rng(width * 7919 + group)
+    n = 20_011
+    ln = (2 * rng.integers(0, (width + 1) // 2, n) + 1).astype(np.int32)
+    tok = np.full((n, width), -1, np.int32)
+    for r in range(n):
+        tok[r, :ln[r]] = rng.integers(0, 2, ln[r])
+    ref_t, ref_l = oracle.unique_walks(tok, ln, group)
+    got_t, got_l = _gpu_unique(tok, ln, group)
+    assert_rows_equal(got_t, got_l, ref_t, ref_l, f"width {width} group {group}")
+
+
 def test_unique_walks_tiny_uniform_corpus():
     w = synth.WORKLOADS["tiny_uniform"]
     say("[unique] tiny_uniform corpus")
