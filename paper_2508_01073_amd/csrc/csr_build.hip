@@ -149,22 +149,27 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
   __syncthreads();
 
   // Wave `wave` owns tile items [wave*kWaveItems, (wave+1)*kWaveItems), visited in order.
+  // All of the wave's loads are issued before any ranking, so they are in
+  // flight together.
   uint32_t key[kRounds];
   int2 pay[kRounds];
   int rank[kRounds];
 #pragma unroll
   for (int r = 0; r < kRounds; ++r) {
     const int local = wave * kWaveItems + r * kWave + lane;
-    const bool valid = local < tile_n;
     const int64_t idx = base + local;
-    uint32_t k = 0;
-    int2 pv = make_int2(0, 0);
-    if (valid) {
-      k = keys_in[idx];
-      pv = kFirst ? make_int2(pred_in[idx], obj_in[idx]) : pay_in[idx];
+    key[r] = 0;
+    pay[r] = make_int2(0, 0);
+    if (local < tile_n) {
+      key[r] = keys_in[idx];
+      pay[r] = kFirst ? make_int2(pred_in[idx], obj_in[idx]) : pay_in[idx];
     }
-    key[r] = k;
-    pay[r] = pv;
+  }
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) {
+    const int local = wave * kWaveItems + r * kWave + lane;
+    const bool valid = local < tile_n;
+    const uint32_t k = key[r];
     const uint32_t d = (k >> shift) & mask;
     // Lanes of this round holding the same digit.
     uint64_t peers = __ballot(valid);

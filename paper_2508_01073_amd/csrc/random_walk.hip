@@ -193,16 +193,15 @@ __global__ __launch_bounds__(kWalkEdgeThreads) void walk_edges_kernel(
       rec[j] = make_int2(v.x, v.y);
     }
   }
+  // The gathers of all items are issued together: an object id out of range is
+  // flagged and read as entity 0, so no load waits on a branch.
 #pragma unroll
   for (int j = 0; j < kWalkEdgeItems; ++j) {
     const int64_t i = base + j * kWalkEdgeThreads;
-    bounds[j] = make_int2(0, 0);
-    if (i < n) {
-      if (uint32_t(rec[j].y) < uint32_t(num_entities))
-        bounds[j] = make_int2(row_ptr[rec[j].y], row_ptr[rec[j].y + 1]);
-      else
-        bad = 1;
-    }
+    const bool ok = uint32_t(rec[j].y) < uint32_t(num_entities);
+    const int32_t o = ok ? rec[j].y : 0;
+    bad |= (i < n && !ok) ? 1 : 0;
+    bounds[j] = i < n ? make_int2(row_ptr[o], row_ptr[o + 1]) : make_int2(0, 0);
   }
 #pragma unroll
   for (int j = 0; j < kWalkEdgeItems; ++j) {
