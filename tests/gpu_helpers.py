@@ -101,6 +101,34 @@ def compare_windows(csr, rp, ed, V, P, starts_np, wpn, depth, seed, tok_dev, len
     return n
 
 
+def compare_all(rp, ed, V, P, starts_np, wpn, depth, seed, tok_dev, len_dev, walk_base=0,
+                piece: int = 1_000_000) -> int:
+    """Compare every row of a device walk batch (walks walk_base ..) with the oracle,
+    which runs in one thread per host core (at most 16) over disjoint walk ranges
+    (each ctypes call runs without the GIL). Returns rows checked."""
+    import concurrent.futures
+    import os
+    tok_h, len_h = tok_dev.cpu().numpy(), len_dev.cpu().numpy()
+    n = len_h.shape[0]
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    chunk = (n + threads - 1) // threads
+
+    def first_bad(lo, hi):
+        for b in range(lo, hi, piece):
+            c = min(piece, hi - b)
+            rt, rl = oracle.random_walks(rp, ed, V, P, starts_np, wpn, depth, seed, walk_base + b, c)
+            if not (np.array_equal(rl, len_h[b:b + c]) and np.array_equal(rt, tok_h[b:b + c])):
+                bad = np.nonzero((rl != len_h[b:b + c]) | np.any(rt != tok_h[b:b + c], axis=1))[0]
+                return b + int(bad[0])
+        return -1
+
+    with concurrent.futures.ThreadPoolExecutor(max_workers=threads) as pool:
+        firsts = list(pool.map(lambda i: first_bad(i * chunk, min(n, (i + 1) * chunk)), range(threads)))
+    bad = [x for x in firsts if x >= 0]
+    assert not bad, f"walk {walk_base + min(bad)} differs from the oracle"
+    return n
+
+
 def check_walk_properties(tok: torch.Tensor, ln: torch.Tensor, starts_dev: torch.Tensor, wpn: int,
                           V: int, P: int, depth: int, walk_begin: int = 0) -> None:
     """Properties every walk row has at any size, checked on the device."""

@@ -15,7 +15,7 @@ import oracle
 import paper_2508_01073_amd as rd
 import synth
 from gpu_helpers import (assert_csr_equal, assert_rows_equal, assert_walk_records, check_walk_properties,
-                         compare_windows, device, gpu_csr, gpu_walks, new_status, plain, say, to_dev)
+                         compare_all, compare_windows, device, gpu_csr, gpu_walks, new_status, plain, say, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -161,6 +161,8 @@ def test_full_size_workload(name):
     win = _windows(num_walks, w.walks_per_node, starts, np.diff(rp), rng)
     n = compare_windows(csr, rp, ed, V, P, starts, w.walks_per_node, w.depth, synth.WALK_SEED, tok, ln, win)
     say(f"[workload] {name}: {n} sampled rows bit-exact")
+    n = compare_all(rp, ed, V, P, starts, w.walks_per_node, w.depth, synth.WALK_SEED, tok, ln)
+    say(f"[workload] {name}: all {n} walks bit-exact")
     # the 8-byte-record path gives the same corpus
     tok2, ln2 = gpu_walks(plain(csr), starts_dev, w.walks_per_node, w.depth, synth.WALK_SEED)
     assert torch.equal(tok2, tok) and torch.equal(ln2, ln)
