@@ -68,6 +68,7 @@ def test_hand_graph_parity(name, depth):
 RANDOM_CASES = [
     (1, 1, 5000), (2, 3, 1), (37, 1, 4096 * 3 + 17), (300, 7, 50_000), (256, 5, 8192),
     (70_000, 11, 100_001), (2**25 + 3, 5, 20_000), (1_000, 20, 4095),
+    (2**18, 9, 300_007), (2**18 + 1, 9, 300_007),  # two 9-bit passes; three 7-bit passes
 ]
 
 
