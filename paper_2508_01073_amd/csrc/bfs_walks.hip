@@ -30,6 +30,7 @@ namespace rdf2v {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kLevelLds = 2048;  // levels of at most this many entities keep their prefix and ids in LDS
 
 struct BfsArgs {
   const int32_t *row_ptr;
@@ -69,6 +70,8 @@ __device__ __forceinline__ uint64_t ld64(const uint64_t *p) {
 
 __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
   __shared__ int32_t scan_scratch[kThreads / kWave];
+  __shared__ int32_t dpre_s[kLevelLds + 1];  // degree prefix of the current level (small levels)
+  __shared__ int32_t ent_s[kLevelLds];       // its entities
   const int t = threadIdx.x;
   const int32_t V = a.num_entities;
   const uint32_t E = uint32_t(a.num_edges);
@@ -114,38 +117,68 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
     int32_t lb = 0, le = 1;
     __syncthreads();
     for (int32_t lev = 0; lev < a.depth && lb < le; ++lev) {
-      // Degree prefix of the level's entities (their (entity, record) pairs are numbered in order).
+      // Degree prefix of the level's entities (their (entity, record) pairs are
+      // numbered in order), in LDS for small levels.
+      const int32_t nlev = le - lb;
+      const bool small = nlev <= kLevelLds;  // uniform across the block
       int32_t carry = 0;
       for (int32_t c0 = lb; c0 < le; c0 += kThreads) {
         const int32_t i = c0 + t;
-        int32_t d = 0;
+        int32_t d = 0, u = 0;
         if (i < le) {
-          const int32_t u = ld(ent + i);
+          u = ld(ent + i);
           const int32_t lo = a.row_ptr[u], hi = a.row_ptr[u + 1];
           if (uint32_t(lo) <= uint32_t(hi) && uint32_t(hi) <= E) d = hi - lo;
           else flags |= RDF2V_STATUS_BAD_CSR;
         }
         int32_t tot;
         const int32_t ex = block_exclusive_scan<kThreads>(d, scan_scratch, tot);
-        if (i < le) st(dpre + (i - lb), carry + ex);
+        if (i < le) {
+          if (small) {
+            dpre_s[i - lb] = carry + ex;
+            ent_s[i - lb] = u;
+          } else {
+            st(dpre + (i - lb), carry + ex);
+          }
+        }
         carry += tot;
       }
       const int32_t total = carry;
-      const int32_t nlev = le - lb;
-      if (t == 0) st(dpre + nlev, total);
+      if (t == 0) {
+        if (small) dpre_s[nlev] = total;
+        else st(dpre + nlev, total);
+      }
+      // Pair q of the level: the level entity (index lo_i) it belongs to, that
+      // entity, and the pair's record index.
+      auto locate = [&](int32_t q, int32_t &lo_i, int32_t &u, uint32_t &j) {
+        lo_i = 0;
+        int32_t hi_i = nlev;  // largest i with dpre[i] <= q
+        if (small) {
+          while (hi_i - lo_i > 1) {
+            const int32_t mid = (lo_i + hi_i) >> 1;
+            if (dpre_s[mid] <= q) lo_i = mid;
+            else hi_i = mid;
+          }
+          u = ent_s[lo_i];
+          j = uint32_t(a.row_ptr[u] + (q - dpre_s[lo_i]));
+        } else {
+          while (hi_i - lo_i > 1) {
+            const int32_t mid = (lo_i + hi_i) >> 1;
+            if (ld(dpre + mid) <= q) lo_i = mid;
+            else hi_i = mid;
+          }
+          u = ld(ent + lb + lo_i);
+          j = uint32_t(a.row_ptr[u] + (q - ld(dpre + lo_i)));
+        }
+      };
       --stamp;
       const uint64_t hi_bits = uint64_t(stamp) << 32;
       __syncthreads();
       // Offers: pair q reaches x; entities already in this root's tree are skipped.
       for (int32_t q = t; q < total; q += kThreads) {
-        int32_t lo_i = 0, hi_i = nlev;  // largest i with dpre[i] <= q
-        while (hi_i - lo_i > 1) {
-          const int32_t mid = (lo_i + hi_i) >> 1;
-          if (ld(dpre + mid) <= q) lo_i = mid;
-          else hi_i = mid;
-        }
-        const int32_t u = ld(ent + lb + lo_i);
-        const uint32_t j = uint32_t(a.row_ptr[u] + (q - ld(dpre + lo_i)));
+        int32_t lo_i, u;
+        uint32_t j;
+        locate(q, lo_i, u, j);
         const int32_t x = edges[j].y;
         if (uint32_t(x) >= uint32_t(V)) {
           flags |= RDF2V_STATUS_ID_OUT_OF_RANGE;
@@ -161,15 +194,10 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
         const int32_t q = c0 + t;
         int32_t win = 0, x = 0, p = 0, node = 0;
         if (q < total) {
-          int32_t lo_i = 0, hi_i = nlev;
-          while (hi_i - lo_i > 1) {
-            const int32_t mid = (lo_i + hi_i) >> 1;
-            if (ld(dpre + mid) <= q) lo_i = mid;
-            else hi_i = mid;
-          }
+          int32_t lo_i, u;
+          uint32_t j;
+          locate(q, lo_i, u, j);
           node = lb + lo_i;
-          const int32_t u = ld(ent + node);
-          const uint32_t j = uint32_t(a.row_ptr[u] + (q - ld(dpre + lo_i)));
           const int2 rec = edges[j];
           p = rec.x;
           x = rec.y;
