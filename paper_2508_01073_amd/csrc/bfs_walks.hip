@@ -18,8 +18,9 @@
 //
 // A persistent grid: workgroup b takes roots b, b + G, ... and owns one slice of
 // the workspace (stamps, offers, tree, degree prefix; about 36 bytes per
-// entity). All loops are bounded by the tree and level sizes; there is no
-// waiting on other workgroups.
+// entity). The first kTreeLds tree positions and small levels are kept in
+// LDS. All loops are bounded by the tree and level sizes; there is no waiting
+// on other workgroups.
 
 #include <algorithm>
 
@@ -30,7 +31,7 @@ namespace rdf2v {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kLevelLds = 2048;  // levels of at most this many entities keep their prefix and ids in LDS
+constexpr int kLevelLds = 1024;  // levels of at most this many entities keep their prefix and row starts in LDS
 
 struct BfsArgs {
   const int32_t *row_ptr;
@@ -68,10 +69,54 @@ __device__ __forceinline__ uint64_t ld64(const uint64_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// The tree of the current root: positions below kTreeLds live in LDS (parent
+// as int16, level and "has a child" as bytes), the rest in the workgroup's
+// global slice. Positions are assigned in the order entities are reached, so
+// small trees and the first levels of big ones stay in LDS.
+constexpr int kTreeLds = 1024;
+
+struct Tree {
+  int32_t *ent_s;
+  int16_t *par_s;
+  int32_t *pred_s;
+  uint8_t *lev_s;
+  uint8_t *child_s;
+  int32_t *ent, *parent, *pred, *level, *has_child;  // global tier
+  __device__ __forceinline__ int32_t get_ent(int32_t i) const { return i < kTreeLds ? ent_s[i] : ld(ent + i); }
+  __device__ __forceinline__ int32_t get_par(int32_t i) const { return i < kTreeLds ? par_s[i] : ld(parent + i); }
+  __device__ __forceinline__ int32_t get_pred(int32_t i) const { return i < kTreeLds ? pred_s[i] : ld(pred + i); }
+  __device__ __forceinline__ int32_t get_lev(int32_t i) const { return i < kTreeLds ? lev_s[i] : ld(level + i); }
+  __device__ __forceinline__ bool leaf(int32_t i) const { return (i < kTreeLds ? child_s[i] : ld(has_child + i)) == 0; }
+  __device__ __forceinline__ void add(int32_t i, int32_t x, int32_t par, int32_t p, int32_t lev) const {
+    if (i < kTreeLds) {
+      ent_s[i] = x;
+      par_s[i] = int16_t(par);  // par < i < kTreeLds
+      pred_s[i] = p;
+      lev_s[i] = uint8_t(lev);
+      child_s[i] = 0;
+    } else {
+      st(ent + i, x);
+      st(parent + i, par);
+      st(pred + i, p);
+      st(level + i, lev);
+      st(has_child + i, 0);
+    }
+  }
+  __device__ __forceinline__ void set_child(int32_t i) const {
+    if (i < kTreeLds) child_s[i] = 1;
+    else st(has_child + i, 1);
+  }
+};
+
 __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
   __shared__ int32_t scan_scratch[kThreads / kWave];
   __shared__ int32_t dpre_s[kLevelLds + 1];  // degree prefix of the current level (small levels)
-  __shared__ int32_t ent_s[kLevelLds];       // its entities
+  __shared__ int32_t rowlo_s[kLevelLds];     // row start of each of its entities
+  __shared__ int32_t t_ent[kTreeLds];
+  __shared__ int32_t t_pred[kTreeLds];
+  __shared__ int16_t t_par[kTreeLds];
+  __shared__ uint8_t t_lev[kTreeLds];
+  __shared__ uint8_t t_child[kTreeLds];
   const int t = threadIdx.x;
   const int32_t V = a.num_entities;
   const uint32_t E = uint32_t(a.num_edges);
@@ -82,12 +127,17 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
   const size_t a4 = align_up(size_t(V) * 4, 256), a8 = align_up(size_t(V) * 8, 256);
   int32_t *mark = reinterpret_cast<int32_t *>(base);
   uint64_t *offer = reinterpret_cast<uint64_t *>(base + a4);
-  int32_t *ent = reinterpret_cast<int32_t *>(base + a4 + a8);
-  int32_t *parent = reinterpret_cast<int32_t *>(base + 2 * a4 + a8);
-  int32_t *pred = reinterpret_cast<int32_t *>(base + 3 * a4 + a8);
-  int32_t *level = reinterpret_cast<int32_t *>(base + 4 * a4 + a8);
-  int32_t *has_child = reinterpret_cast<int32_t *>(base + 5 * a4 + a8);
   int32_t *dpre = reinterpret_cast<int32_t *>(base + 6 * a4 + a8);
+  const Tree tree{t_ent,
+                  t_par,
+                  t_pred,
+                  t_lev,
+                  t_child,
+                  reinterpret_cast<int32_t *>(base + a4 + a8),
+                  reinterpret_cast<int32_t *>(base + 2 * a4 + a8),
+                  reinterpret_cast<int32_t *>(base + 3 * a4 + a8),
+                  reinterpret_cast<int32_t *>(base + 4 * a4 + a8),
+                  reinterpret_cast<int32_t *>(base + 5 * a4 + a8)};
 
   // Each workgroup initialises its own slice once per call.
   for (int32_t v = t; v < V; v += kThreads) {
@@ -107,27 +157,24 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
       continue;  // uniform: every lane skips the same root
     }
     if (t == 0) {
-      st(ent, root);
-      st(parent, -1);
-      st(pred, -1);
-      st(level, 0);
-      st(has_child, 0);
+      tree.add(0, root, -1, -1, 0);
       st(mark + root, mark_id);
     }
     int32_t lb = 0, le = 1;
     __syncthreads();
     for (int32_t lev = 0; lev < a.depth && lb < le; ++lev) {
       // Degree prefix of the level's entities (their (entity, record) pairs are
-      // numbered in order), in LDS for small levels.
+      // numbered in order), with the row starts, in LDS for small levels.
       const int32_t nlev = le - lb;
       const bool small = nlev <= kLevelLds;  // uniform across the block
       int32_t carry = 0;
       for (int32_t c0 = lb; c0 < le; c0 += kThreads) {
         const int32_t i = c0 + t;
-        int32_t d = 0, u = 0;
+        int32_t d = 0, lo = 0;
         if (i < le) {
-          u = ld(ent + i);
-          const int32_t lo = a.row_ptr[u], hi = a.row_ptr[u + 1];
+          const int32_t u = tree.get_ent(i);
+          lo = a.row_ptr[u];
+          const int32_t hi = a.row_ptr[u + 1];
           if (uint32_t(lo) <= uint32_t(hi) && uint32_t(hi) <= E) d = hi - lo;
           else flags |= RDF2V_STATUS_BAD_CSR;
         }
@@ -136,7 +183,7 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
         if (i < le) {
           if (small) {
             dpre_s[i - lb] = carry + ex;
-            ent_s[i - lb] = u;
+            rowlo_s[i - lb] = lo;
           } else {
             st(dpre + (i - lb), carry + ex);
           }
@@ -148,9 +195,9 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
         if (small) dpre_s[nlev] = total;
         else st(dpre + nlev, total);
       }
-      // Pair q of the level: the level entity (index lo_i) it belongs to, that
-      // entity, and the pair's record index.
-      auto locate = [&](int32_t q, int32_t &lo_i, int32_t &u, uint32_t &j) {
+      // Pair q of the level: the level entity (index lo_i) it belongs to and the
+      // pair's record index.
+      auto locate = [&](int32_t q, int32_t &lo_i, uint32_t &j) {
         lo_i = 0;
         int32_t hi_i = nlev;  // largest i with dpre[i] <= q
         if (small) {
@@ -159,15 +206,14 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
             if (dpre_s[mid] <= q) lo_i = mid;
             else hi_i = mid;
           }
-          u = ent_s[lo_i];
-          j = uint32_t(a.row_ptr[u] + (q - dpre_s[lo_i]));
+          j = uint32_t(rowlo_s[lo_i] + (q - dpre_s[lo_i]));
         } else {
           while (hi_i - lo_i > 1) {
             const int32_t mid = (lo_i + hi_i) >> 1;
             if (ld(dpre + mid) <= q) lo_i = mid;
             else hi_i = mid;
           }
-          u = ld(ent + lb + lo_i);
+          const int32_t u = tree.get_ent(lb + lo_i);
           j = uint32_t(a.row_ptr[u] + (q - ld(dpre + lo_i)));
         }
       };
@@ -176,9 +222,9 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
       __syncthreads();
       // Offers: pair q reaches x; entities already in this root's tree are skipped.
       for (int32_t q = t; q < total; q += kThreads) {
-        int32_t lo_i, u;
+        int32_t lo_i;
         uint32_t j;
-        locate(q, lo_i, u, j);
+        locate(q, lo_i, j);
         const int32_t x = edges[j].y;
         if (uint32_t(x) >= uint32_t(V)) {
           flags |= RDF2V_STATUS_ID_OUT_OF_RANGE;
@@ -194,9 +240,9 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
         const int32_t q = c0 + t;
         int32_t win = 0, x = 0, p = 0, node = 0;
         if (q < total) {
-          int32_t lo_i, u;
+          int32_t lo_i;
           uint32_t j;
-          locate(q, lo_i, u, j);
+          locate(q, lo_i, j);
           node = lb + lo_i;
           const int2 rec = edges[j];
           p = rec.x;
@@ -207,12 +253,8 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
         const int32_t ex = block_exclusive_scan<kThreads>(win, scan_scratch, tot);
         if (win) {
           const int32_t pos = le + added + ex;
-          st(ent + pos, x);
-          st(parent + pos, node);
-          st(pred + pos, p);
-          st(level + pos, lev + 1);
-          st(has_child + pos, 0);
-          st(has_child + node, 1);
+          tree.add(pos, x, node, p, lev + 1);
+          tree.set_child(node);
           st(mark + x, mark_id);
         }
         added += tot;
@@ -225,18 +267,18 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
     int32_t leaves = 0;
     for (int32_t c0 = 0; c0 < le; c0 += kThreads) {
       const int32_t i = c0 + t;
-      const int32_t leaf = i < le ? (ld(has_child + i) == 0) : 0;
+      const int32_t leaf = i < le ? int32_t(tree.leaf(i)) : 0;
       int32_t tot;
       const int32_t ex = block_exclusive_scan<kThreads>(leaf, scan_scratch, tot);
       const int32_t idx = leaves + ex;
       if (leaf && idx < a.max_walks) {
-        const int32_t h = ld(level + i);
+        const int32_t h = tree.get_lev(i);
         int32_t *row = a.tokens + (r * a.max_walks + idx) * width;
         int32_t node = i;
         for (int32_t step = h; step >= 1; --step) {
-          row[2 * step] = ld(ent + node);
-          row[2 * step - 1] = V + ld(pred + node);
-          node = ld(parent + node);
+          row[2 * step] = tree.get_ent(node);
+          row[2 * step - 1] = V + tree.get_pred(node);
+          node = tree.get_par(node);
         }
         row[0] = root;
         for (int64_t j = 2 * int64_t(h) + 1; j < width; ++j) row[j] = -1;

@@ -66,6 +66,23 @@ def test_random_multigraphs(V, T, depth, seed):
     _compare(csr, rp, ed, V, P, roots, depth, 7, f"V={V} truncated")
 
 
+def test_big_levels_and_trees():
+    # mean out-degree 20: levels of hundreds and thousands of entities and trees
+    # of up to ~20k, past the part of the tree and of a level that is kept in LDS
+    say("[bfs] V=20000 T=400000 depth 4, big levels and trees")
+    V, P, T = 20_000, 5, 400_000
+    rng = np.random.default_rng(11)
+    s = rng.integers(0, V, T).astype(np.int32)
+    p = rng.integers(0, P, T).astype(np.int32)
+    o = rng.integers(0, V, T).astype(np.int32)
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    roots = rng.integers(0, V, 24).astype(np.int32)
+    counts = _compare(csr, rp, ed, V, P, roots, 4, V, "big levels")
+    assert counts.max() > 5000
+    _compare(csr, rp, ed, V, P, roots, 3, 1500, "big levels truncated")
+
+
 def test_tiny_uniform_all_roots():
     w = synth.WORKLOADS["tiny_uniform"]
     say("[bfs] tiny_uniform, every entity as root, depth 3")
