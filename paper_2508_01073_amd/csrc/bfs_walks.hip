@@ -5,22 +5,24 @@
 // The tree is the one a queue-order BFS builds: the entities of a level are
 // expanded in the order they were reached, each through its out-edge records in
 // CSR order, and an entity gets as parent the first (entity, record) that
-// reaches it. The kernel gets the same tree level-synchronously:
+// reaches it. The kernels get the same tree level-synchronously:
 //   * the (entity, record) pairs of a level are numbered q = 0, 1, ... in
 //     exactly that order (a block scan of the level's degrees);
-//   * every pair that reaches an entity not yet in the tree offers
-//     (stamp << 32 | q) to that entity with a 64-bit atomicMin, so the smallest
-//     q wins; stamps fall with every (root, level) a workgroup processes, so
-//     offers left from earlier levels or roots always lose;
+//   * every pair that reaches an entity not yet in the tree offers q to that
+//     entity with an atomic minimum, so the smallest q wins;
 //   * the winners, in q order (a block scan), are the next level.
 // Leaves are then ranked in the order reached and the first max_walks become
 // rows root, V+p_1, v_1, ..., leaf.
 //
-// A persistent grid: workgroup b takes roots b, b + G, ... and owns one slice of
-// the workspace (stamps, offers, tree, degree prefix; about 36 bytes per
-// entity). The first kTreeLds tree positions and small levels are kept in
-// LDS. All loops are bounded by the tree and level sizes; there is no waiting
-// on other workgroups.
+// Three passes. Two LDS tiers run a root in LDS alone: the tree, the level's
+// degree prefix and an open-addressing hash table of the entities reached so
+// far (tree members and this level's offers). Every root goes to the small
+// tier first; a root whose tree outgrows a tier is abandoned there and queued
+// for the next one. The last pass, a persistent grid of workgroups that each
+// own a slice of the workspace (per-entity stamps and offers, the tree beyond
+// its first kTreeLds positions; about 36 bytes per entity), reruns the roots
+// neither tier could hold from scratch. All loops are bounded by the tree and
+// level sizes or the table size; there is no waiting on other workgroups.
 
 #include <algorithm>
 
@@ -41,7 +43,9 @@ struct BfsArgs {
   int32_t *lens;
   int32_t *counts;
   int32_t *status;
-  char *workspace;
+  int32_t *queue_counts;  // [6]: lengths of the queues below, then how far each has been taken
+  int32_t *queue[3];      // roots (indices into roots) LDS tier i could not hold
+  char *workspace;        // slices of the workspace pass
   size_t slice_bytes;
   int64_t num_roots;
   int64_t num_edges;
@@ -56,6 +60,9 @@ struct BfsArgs {
 inline size_t slice_bytes(int64_t V) {
   return align_up(size_t(V) * 4, 256) * 6 + align_up(size_t(V) * 8, 256) + align_up(size_t(V + 1) * 4, 256);
 }
+
+// Workspace: the queue counters, three queues (one int32 per root each), the slices.
+inline size_t queue_bytes(int64_t num_roots) { return 256 + 3 * align_up(size_t(num_roots) * 4, 256); }
 
 // Scratch arrays are shared by the whole workgroup and written by atomics or by
 // other lanes; agent-scope relaxed accesses keep every read at L2.
@@ -108,6 +115,472 @@ struct Tree {
   }
 };
 
+// ---------------------------------------------------------------------------
+// First pass: one root at a time per workgroup, all state in LDS.
+
+// Three LDS tiers of growing capacity and LDS footprint: one wave per root
+// (about 6.3 KB of LDS, 24 workgroups per CU), 256 threads (about 25 KB, 6
+// per CU) and 512 threads (about 50 KB, 3 per CU). A root goes to the next
+// tier when it outgrows one. All keep VGPRs <= 80 for six waves per SIMD (the
+// big tier spills a few registers for its four rounds).
+struct TinyTier {
+  static constexpr int kThreads = 64;
+  static constexpr int kRounds = 2;
+  static constexpr int kLog = 9;
+  static constexpr int kCap = 384;
+  static constexpr int kTreeCap = 96;
+  static constexpr int kWavesPerSimd = 6;
+  static constexpr int kPerCu = 24;  // workgroups per CU (LDS-bound)
+};
+struct SmallTier {
+  static constexpr int kThreads = 256;
+  static constexpr int kRounds = 2;     // rounds of kThreads pairs whose records are loaded together
+  static constexpr int kLog = 11;       // hash table of 2^kLog slots
+  static constexpr int kCap = 1536;     // most entities a root may reach here
+  static constexpr int kTreeCap = 384;  // most of them above the depth limit (kept as tree nodes)
+  static constexpr int kWavesPerSimd = 6;
+  static constexpr int kPerCu = 6;
+};
+struct BigTier {
+  static constexpr int kThreads = 512;
+  static constexpr int kRounds = 4;
+  static constexpr int kLog = 12;
+  static constexpr int kCap = 3072;
+  static constexpr int kTreeCap = 768;
+  static constexpr int kWavesPerSimd = 6;
+  static constexpr int kPerCu = 3;
+};
+constexpr int32_t kFreeSlot = -1;
+constexpr uint32_t kNoOffer = 0xFFFFFFFFu;
+
+// Fibonacci hashing of an entity id to one of 2^kLog slots.
+template <int kLog>
+__device__ __forceinline__ int32_t entity_slot(int32_t x) {
+  return int32_t((uint32_t(x) * 0x9E3779B1u) >> (32 - kLog));
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave with DPP moves: shifts by
+// 1, 2, 4 and 8 lanes inside each row of 16, then the last lane of row 0 and of
+// row 2 added to rows 1 and 3, then the last lane of row 1 added to rows 2 and
+// 3 (the row-broadcast scan of AMD's GCN cross-lane notes). Lanes with no
+// source lane or in masked rows add 0.
+__device__ __forceinline__ int32_t wave_inclusive_sum(int32_t x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15 into rows 1 and 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31 into rows 2 and 3
+  return x;
+}
+
+__device__ __forceinline__ int32_t wave_sum(int32_t v) {
+  return __builtin_amdgcn_readlane(wave_inclusive_sum(v), kWave - 1);
+}
+
+__device__ __forceinline__ int32_t wave_index() { return __builtin_amdgcn_readfirstlane(int32_t(threadIdx.x) / kWave); }
+
+// Set bits of a wave-wide mask below the calling lane.
+__device__ __forceinline__ int32_t lanes_below(uint64_t b) {
+  return int32_t(__builtin_amdgcn_mbcnt_hi(uint32_t(b >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(b), 0u)));
+}
+
+// Exclusive prefix sum over the block (one value per thread) and its total.
+// Two barriers; scratch holds NT/64 ints.
+template <int NT>
+__device__ __forceinline__ int32_t block_scan(int32_t x, int32_t *scratch, int32_t &total) {
+  constexpr int W = NT / kWave;
+  const int32_t inc = wave_inclusive_sum(x);
+  if constexpr (W == 1) {
+    total = __builtin_amdgcn_readlane(inc, kWave - 1);
+    return inc - x;
+  } else {
+    const int lane = lane_id();
+    const int32_t w = wave_index();
+    if (lane == kWave - 1) scratch[w] = inc;
+    __syncthreads();
+    const int32_t waves = wave_inclusive_sum(lane < W ? scratch[lane] : 0);
+    __syncthreads();
+    total = __builtin_amdgcn_readlane(waves, W - 1);
+    return (w > 0 ? __builtin_amdgcn_readlane(waves, w - 1) : 0) + inc - x;
+  }
+}
+
+// Ranks, in pair order, the flagged pairs of a chunk whose round k holds pair
+// c0 + k*NT + threadIdx.x: rank[k] counts the flagged pairs before it in the
+// chunk; `total` is their number. Two barriers; cnt_s holds R * NT/64 ints.
+template <int NT, int R>
+__device__ __forceinline__ void rank_chunk(uint32_t mask, int32_t (&rank)[R], int32_t &total, int32_t *cnt_s) {
+  constexpr int W = NT / kWave;
+  static_assert(R * W <= kWave, "one count per lane");
+  const int lane = lane_id();
+  const int32_t w = wave_index();
+  uint64_t b[R];
+#pragma unroll
+  for (int k = 0; k < R; ++k) b[k] = __ballot((mask >> k) & 1u);
+  // counts in pair order: round-major, then wave
+  if (lane == 0) {
+#pragma unroll
+    for (int k = 0; k < R; ++k) cnt_s[k * W + w] = __popcll(b[k]);
+  }
+  __syncthreads();
+  const int32_t inc = wave_inclusive_sum(lane < R * W ? cnt_s[lane] : 0);
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int32_t idx = k * W + w;
+    rank[k] = (idx > 0 ? __builtin_amdgcn_readlane(inc, idx - 1) : 0) + lanes_below(b[k]);
+  }
+  total = __builtin_amdgcn_readlane(inc, R * W - 1);
+}
+
+// Table entries: key = entity, value = 0 for a tree member, else 1 + the
+// smallest pair index of the current level that reached it. Every entity
+// inserted during a level's offers has a winning pair, so after the level the
+// entry count is the tree size.
+//
+// Entities at the depth limit are leaves: they are not stored as tree nodes.
+// Their pairs are walked twice more instead, once to mark which nodes of the
+// level above get a child, and once, after the stored leaves are ranked, to
+// write their walks in pair order.
+//
+// The pairs of a level are taken in chunks of R rounds of NT consecutive
+// pairs; a thread loads the records of its R pairs together. A level of at
+// most one chunk keeps its records (and winners) in registers for all its
+// passes.
+//
+// Without in_queue, workgroup b takes roots b, b + G, ...; with it, the
+// workgroups take its in_count entries one at a time through the counter
+// `taken`. Roots the tier cannot hold are appended to out_queue.
+template <int NT, int R, int kLog, int kCap, int kTreeCap, int kWpe>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kWpe))) void bfs_lds_kernel(
+    const BfsArgs a, const int32_t *in_queue, const int32_t *in_count, int32_t *taken, int32_t *out_queue,
+    int32_t *out_count) {
+  constexpr int kSlots = 1 << kLog;
+  constexpr int32_t kChunk = NT * R;
+  static_assert(kCap < kSlots && kTreeCap <= kCap && kTreeCap <= 32767, "table and tree sizes");
+  static_assert(kSlots % (4 * NT) == 0, "the table is cleared four slots per thread at a time");
+  static_assert(R <= 32, "win masks are 32-bit");
+  __shared__ int32_t scan_scratch[R * (NT / kWave)];
+  __shared__ __align__(16) int32_t h_key[kSlots];
+  __shared__ __align__(16) uint32_t h_val[kSlots];
+  __shared__ int32_t t_ent[kTreeCap];
+  __shared__ int32_t t_pred[kTreeCap];
+  __shared__ int16_t t_par[kTreeCap];
+  __shared__ uint8_t t_lev[kTreeCap];
+  __shared__ uint8_t t_child[kTreeCap];
+  __shared__ int32_t t_lo[kTreeCap];        // CSR row start of each tree node
+  __shared__ int32_t t_deg[kTreeCap];       // and its out-degree (0 for a bad row)
+  __shared__ int32_t dpre_s[kTreeCap + 1];  // degree prefix of the level being expanded
+  __shared__ int32_t used_s;                // table entries
+  __shared__ int32_t overflow_s;
+  __shared__ int32_t next_s;
+  const int t = threadIdx.x;
+  const int32_t V = a.num_entities;
+  const uint32_t E = uint32_t(a.num_edges);
+  const int64_t width = 2 * int64_t(a.depth) + 1;
+  const int2 *edges = reinterpret_cast<const int2 *>(a.edges);
+
+  // Slot of x, inserting it if absent (then `inserted` is incremented); -1
+  // when the table is full (the root is then left to the next tier). The
+  // entry count is checked against kCap once all offers of a level are in.
+  auto claim = [&](int32_t x, int32_t &inserted) -> int32_t {
+    int32_t s = entity_slot<kLog>(x);
+    for (int n = 0; n < kSlots; ++n) {
+      const int32_t k = __hip_atomic_load(h_key + s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (k == x) return s;
+      if (k == kFreeSlot) {
+        const int32_t old = atomicCAS(h_key + s, kFreeSlot, x);
+        if (old == kFreeSlot) {
+          ++inserted;
+          return s;
+        }
+        if (old == x) return s;
+      }
+      s = (s + 1) & (kSlots - 1);
+    }
+    overflow_s = 1;
+    return -1;
+  };
+  auto find = [&](int32_t x) -> int32_t {
+    int32_t s = entity_slot<kLog>(x);
+    for (int n = 0; n < kSlots; ++n) {
+      const int32_t k = h_key[s];
+      if (k == x) return s;
+      if (k == kFreeSlot) break;
+      s = (s + 1) & (kSlots - 1);
+    }
+    return -1;
+  };
+
+  int flags = 0;
+  const int64_t n_in = in_queue != nullptr ? int64_t(*in_count) : a.num_roots;
+  if (int64_t(blockIdx.x) >= n_in) return;  // uniform; an empty queue costs one load per workgroup
+  for (int64_t k_in = blockIdx.x;; k_in += gridDim.x) {
+    if (in_queue != nullptr) {  // uniform
+      if (t == 0) next_s = atomicAdd(taken, 1);
+      __syncthreads();
+      k_in = next_s;
+      __syncthreads();
+    }
+    if (k_in >= n_in) break;
+    const int64_t r = in_queue != nullptr ? int64_t(in_queue[k_in]) : k_in;
+    const int32_t root = a.roots[r];
+    if (uint32_t(root) >= uint32_t(V)) {
+      if (t == 0) a.counts[r] = 0;
+      flags |= RDF2V_STATUS_ID_OUT_OF_RANGE;
+      continue;  // uniform: every lane skips the same root
+    }
+    for (int i = t; i < kSlots / 4; i += NT) {
+      reinterpret_cast<int4 *>(h_key)[i] = make_int4(kFreeSlot, kFreeSlot, kFreeSlot, kFreeSlot);
+      reinterpret_cast<uint4 *>(h_val)[i] = make_uint4(kNoOffer, kNoOffer, kNoOffer, kNoOffer);
+    }
+    __syncthreads();
+    if (t == 0) {
+      const int32_t lo = a.row_ptr[root], hi = a.row_ptr[root + 1];
+      const bool ok = uint32_t(lo) <= uint32_t(hi) && uint32_t(hi) <= E;
+      if (!ok) flags |= RDF2V_STATUS_BAD_CSR;
+      t_lo[0] = lo;
+      t_deg[0] = ok ? hi - lo : 0;
+      const int32_t s0 = entity_slot<kLog>(root);
+      h_key[s0] = root;
+      h_val[s0] = 0;
+      used_s = 1;
+      overflow_s = 0;
+      t_ent[0] = root;
+      t_pred[0] = -1;
+      t_par[0] = -1;
+      t_lev[0] = 0;
+      t_child[0] = 0;
+    }
+    __syncthreads();
+    int32_t lb = 0, le = 1;      // the level being expanded: tree nodes [lb, le)
+    int32_t nlev = 0, total = 0;  // its size and its number of (entity, record) pairs
+    int32_t last_wins = 0;       // entities reached at the depth limit
+    bool overflow = false;
+    // The thread's pairs of the chunk at c0 (round k: pair c0 + k*NT + t): level
+    // entity index (-1 past the end), record, and table slot of the record's
+    // entity (-1 if none).
+    int32_t node_k[R];
+    int2 rec_k[R];
+    int32_t slot_k[R];
+    auto load_chunk = [&](int32_t c0) {
+#pragma unroll
+      for (int k = 0; k < R; ++k) {
+        node_k[k] = -1;
+        rec_k[k] = make_int2(0, -1);
+      }
+      if (c0 + wave_index() * kWave >= total) return;  // uniform: no pair of this wave in the chunk
+      // largest i with dpre[i] <= q, by halving steps from the top bit of nlev
+      int32_t lo[R];
+#pragma unroll
+      for (int k = 0; k < R; ++k) lo[k] = 0;
+      for (int32_t step = int32_t(1u << (31 - __builtin_clz(uint32_t(nlev)))); step > 0; step >>= 1) {
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+          const int32_t m = lo[k] + step;
+          if (m < nlev && dpre_s[m] <= c0 + k * NT + t) lo[k] = m;
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < R; ++k) {
+        const int32_t q = c0 + k * NT + t;
+        node_k[k] = q < total ? lo[k] : -1;
+        rec_k[k] = q < total ? edges[uint32_t(t_lo[lb + lo[k]] + (q - dpre_s[lo[k]]))] : make_int2(0, -1);
+      }
+    };
+    // Bit k set: the thread's round-k pair reaches its entity first. With
+    // `known`, slot_k holds the slots from this chunk's offers; else they are
+    // looked up.
+    auto winners = [&](int32_t c0, bool known) -> uint32_t {
+      uint32_t m = 0;
+#pragma unroll
+      for (int k = 0; k < R; ++k) {
+        if (!known) slot_k[k] = node_k[k] >= 0 && uint32_t(rec_k[k].y) < uint32_t(V) ? find(rec_k[k].y) : -1;
+        if (slot_k[k] >= 0 && h_val[slot_k[k]] == uint32_t(c0 + k * NT + t) + 1u) m |= 1u << k;
+      }
+      return m;
+    };
+    uint32_t last_mask = 0;  // winners of a one-chunk last level
+    for (int32_t lev = 0; lev < a.depth && lb < le; ++lev) {
+      nlev = le - lb;  // le <= kTreeCap
+      // Degree prefix of the level (rows were read when its nodes were added).
+      int32_t carry = 0;
+      for (int32_t c0 = lb; c0 < le; c0 += NT) {
+        const int32_t i = c0 + t;
+        int32_t tot;
+        const int32_t ex = block_scan<NT>(i < le ? t_deg[i] : 0, scan_scratch, tot);
+        if (i < le) dpre_s[i - lb] = carry + ex;
+        carry += tot;
+      }
+      total = carry;
+      if (t == 0) dpre_s[nlev] = total;
+      __syncthreads();
+      const bool one_chunk = total <= kChunk;  // uniform: records stay in registers
+      // Offers (tree members hold 0 and ignore them).
+      bool full = false;
+      int32_t inserted = 0;
+      for (int32_t c0 = 0; c0 < total && !full; c0 += kChunk) {
+        load_chunk(c0);
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+          slot_k[k] = -1;
+          if (full || node_k[k] < 0) continue;
+          const int32_t x = rec_k[k].y;
+          if (uint32_t(x) >= uint32_t(V)) {
+            flags |= RDF2V_STATUS_ID_OUT_OF_RANGE;
+            continue;
+          }
+          const int32_t s = claim(x, inserted);
+          if (s < 0) {
+            full = true;
+          } else {
+            slot_k[k] = s;
+            atomicMin(h_val + s, uint32_t(c0 + k * NT + t) + 1u);
+          }
+        }
+      }
+      inserted = wave_sum(inserted);
+      if (lane_id() == 0 && inserted > 0) atomicAdd(&used_s, inserted);
+      __syncthreads();
+      const bool last = lev + 1 == a.depth;
+      if (overflow_s || used_s > (last ? kCap : kTreeCap)) {  // uniform
+        overflow = true;
+        break;
+      }
+      if (last) {
+        // Nodes of this level with a winning pair are not leaves.
+        int32_t n_wins = 0;
+        for (int32_t c0 = 0; c0 < total; c0 += kChunk) {
+          if (!one_chunk) load_chunk(c0);
+          const uint32_t m = winners(c0, one_chunk);
+#pragma unroll
+          for (int k = 0; k < R; ++k)
+            if (m & (1u << k)) t_child[lb + node_k[k]] = 1;
+          n_wins += __popc(m);
+          last_mask = m;
+        }
+        {
+          int32_t all;
+          (void)block_scan<NT>(n_wins, scan_scratch, all);
+          last_wins = all;
+        }
+        break;  // lb, le, nlev, total (and a one-chunk level's records) stay for the rows
+      }
+      // Winners in pair order become the next level.
+      int32_t added = 0;
+      for (int32_t c0 = 0; c0 < total; c0 += kChunk) {
+        if (!one_chunk) load_chunk(c0);
+        int32_t rank[R], tot, row_lo[R], row_hi[R];
+        const uint32_t m = winners(c0, one_chunk);
+#pragma unroll
+        for (int k = 0; k < R; ++k) {  // the new nodes' rows, in flight across the ranking
+          row_lo[k] = row_hi[k] = 0;
+          if (m & (1u << k)) {
+            row_lo[k] = a.row_ptr[rec_k[k].y];
+            row_hi[k] = a.row_ptr[rec_k[k].y + 1];
+          }
+        }
+        rank_chunk<NT, R>(m, rank, tot, scan_scratch);
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+          if (m & (1u << k)) {
+            const int32_t pos = le + added + rank[k];  // < used_s <= kTreeCap
+            const int32_t node = lb + node_k[k];
+            const bool ok = uint32_t(row_lo[k]) <= uint32_t(row_hi[k]) && uint32_t(row_hi[k]) <= E;
+            if (!ok) flags |= RDF2V_STATUS_BAD_CSR;
+            t_ent[pos] = rec_k[k].y;
+            t_pred[pos] = rec_k[k].x;
+            t_par[pos] = int16_t(node);
+            t_lev[pos] = uint8_t(lev + 1);
+            t_child[pos] = 0;
+            t_lo[pos] = row_lo[k];
+            t_deg[pos] = ok ? row_hi[k] - row_lo[k] : 0;
+            t_child[node] = 1;
+            h_val[slot_k[k]] = 0;
+          }
+        }
+        added += tot;
+      }
+      lb = le;
+      le += added;
+      __syncthreads();
+    }
+    if (overflow) {
+      if (t == 0) out_queue[atomicAdd(out_count, 1)] = int32_t(r);
+      continue;  // the clearing loop of the next root starts after this root's last barrier
+    }
+    // Walk rows: root, then the tokens of `node` and its ancestors up to level h.
+    auto write_path = [&](int32_t *row, int32_t node, int32_t h) {
+      for (int32_t step = h; step >= 1; --step) {
+        row[2 * step] = t_ent[node];
+        row[2 * step - 1] = V + t_pred[node];
+        node = t_par[node];
+      }
+      row[0] = root;
+    };
+    // Leaves in the order reached, the stored tree nodes first: the first
+    // max_walks become walks.
+    int32_t leaves = 0;
+    for (int32_t c0 = 0; c0 < le; c0 += NT) {
+      const int32_t i = c0 + t;
+      const int32_t leaf = i < le ? int32_t(t_child[i] == 0) : 0;
+      int32_t tot;
+      const int32_t ex = block_scan<NT>(leaf, scan_scratch, tot);
+      const int32_t idx = leaves + ex;
+      if (leaf && idx < a.max_walks) {
+        const int32_t h = t_lev[i];
+        int32_t *row = a.tokens + (r * a.max_walks + idx) * width;
+        write_path(row, i, h);
+        for (int64_t j = 2 * int64_t(h) + 1; j < width; ++j) row[j] = -1;
+        a.lens[r * a.max_walks + idx] = 2 * h + 1;
+      }
+      leaves += tot;
+    }
+    // Then the entities at the depth limit, in pair order.
+    if (last_wins > 0 && leaves < a.max_walks) {
+      const bool one_chunk = total <= kChunk;
+      int32_t added = 0;
+      for (int32_t c0 = 0; c0 < total; c0 += kChunk) {
+        uint32_t m = last_mask;
+        if (!one_chunk) {
+          load_chunk(c0);
+          m = winners(c0, false);
+        }
+        int32_t rank[R], tot;
+        rank_chunk<NT, R>(m, rank, tot, scan_scratch);
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+          const int32_t idx = leaves + added + rank[k];
+          if ((m & (1u << k)) && idx < a.max_walks) {
+            int32_t *row = a.tokens + (r * a.max_walks + idx) * width;
+            row[2 * a.depth] = rec_k[k].y;
+            row[2 * a.depth - 1] = V + rec_k[k].x;
+            write_path(row, lb + node_k[k], a.depth - 1);
+            a.lens[r * a.max_walks + idx] = int32_t(width);
+          }
+        }
+        added += tot;
+        if (leaves + added >= a.max_walks) break;  // uniform
+      }
+    }
+    leaves += last_wins;
+    if (t == 0) {
+      a.counts[r] = min(leaves, a.max_walks);
+      if (leaves > a.max_walks) flags |= RDF2V_STATUS_CAPACITY;
+    }
+    __syncthreads();  // the LDS is reused by the next root
+  }
+  if (flags && a.status != nullptr) atomicOr(a.status, flags);
+}
+
+__global__ void bfs_queue_reset_kernel(int32_t *queue_counts) {
+  if (threadIdx.x < 6) queue_counts[threadIdx.x] = 0;
+}
+
+// ---------------------------------------------------------------------------
+// Second pass: the queued roots, with per-workgroup slices of the workspace.
+
 __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
   __shared__ int32_t scan_scratch[kThreads / kWave];
   __shared__ int32_t dpre_s[kLevelLds + 1];  // degree prefix of the current level (small levels)
@@ -139,6 +612,8 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
                   reinterpret_cast<int32_t *>(base + 4 * a4 + a8),
                   reinterpret_cast<int32_t *>(base + 5 * a4 + a8)};
 
+  const int32_t queued = a.queue_counts[2];
+  if (int32_t(blockIdx.x) >= queued) return;  // uniform, before any barrier
   // Each workgroup initialises its own slice once per call.
   for (int32_t v = t; v < V; v += kThreads) {
     st(mark + v, -1);
@@ -148,7 +623,8 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
 
   uint32_t stamp = 0xFFFFFFFEu;  // falls by one per (root, level) of this workgroup
   int flags = 0;
-  for (int64_t r = blockIdx.x; r < a.num_roots; r += gridDim.x) {
+  for (int32_t k = blockIdx.x; k < queued; k += gridDim.x) {
+    const int64_t r = a.queue[2][k];
     const int32_t root = a.roots[r];
     const int32_t mark_id = int32_t(r);
     if (uint32_t(root) >= uint32_t(V)) {
@@ -297,8 +773,39 @@ __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
 
 }  // namespace
 
+template <class T>
+void launch_tier(const BfsArgs &a, const int32_t *in_q, const int32_t *in_c, int32_t *taken, int32_t *out_q,
+                 int32_t *out_c, int64_t grid, hipStream_t stream) {
+  bfs_lds_kernel<T::kThreads, T::kRounds, T::kLog, T::kCap, T::kTreeCap, T::kWavesPerSimd>
+      <<<dim3(unsigned(grid)), dim3(T::kThreads), 0, stream>>>(a, in_q, in_c, taken, out_q, out_c);
+}
+
+// The tier every root starts in: the smallest whose capacity is at least twice
+// the expected tree size, 1 + d + ... + d^depth for the mean out-degree d
+// (at most V). Only the speed depends on this choice: a root that outgrows a
+// tier is rerun by the next.
+int bfs_first_tier(int32_t num_entities, int64_t num_edges, int64_t num_roots, int32_t depth) {
+  const double d = num_entities > 0 ? double(num_edges) / double(num_entities) : 0.0;
+  double est = 1.0, level = 1.0;
+  for (int32_t l = 0; l < depth && est < 1e9; ++l) {
+    level *= d;
+    est += level;
+  }
+  est = std::min(est, double(num_entities));
+  int first = 2.0 * est <= TinyTier::kCap ? 0 : 2.0 * est <= SmallTier::kCap ? 1 : 2;
+  // When a tier with more threads per root holds every root on the chip at
+  // once, the extra threads shorten each root instead of waiting.
+  int cus = 0, dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus = 0;
+  if (first < 2 && num_roots <= int64_t(cus) * BigTier::kPerCu) first = 2;
+  else if (first < 1 && num_roots <= int64_t(cus) * SmallTier::kPerCu) first = 1;
+  return first;
+}
+
 int64_t bfs_walks_grid(int32_t num_entities, int64_t num_roots) {
-  // Enough workgroups to fill the chip, at most ~4 GiB of slices.
+  // Second pass: enough workgroups to fill the chip, at most ~4 GiB of slices.
   const int64_t per = int64_t(slice_bytes(num_entities));
   int64_t g = std::max<int64_t>(1, (int64_t(1) << 32) / std::max<int64_t>(per, 1));
   g = std::min<int64_t>(g, 2048);
@@ -307,7 +814,7 @@ int64_t bfs_walks_grid(int32_t num_entities, int64_t num_roots) {
 }
 
 size_t bfs_walks_workspace_bytes(int32_t num_entities, int64_t num_roots) {
-  return size_t(bfs_walks_grid(num_entities, num_roots)) * slice_bytes(num_entities);
+  return queue_bytes(num_roots) + size_t(bfs_walks_grid(num_entities, num_roots)) * slice_bytes(num_entities);
 }
 
 rdf2v_status launch_bfs_walks(const int32_t *row_ptr, const int32_t *edges, int64_t num_edges,
@@ -316,6 +823,7 @@ rdf2v_status launch_bfs_walks(const int32_t *row_ptr, const int32_t *edges, int6
                               int32_t *len_out, int32_t *counts_out, void *workspace, int32_t *status_dev,
                               hipStream_t stream) {
   if (num_roots == 0) return RDF2V_OK;
+  char *ws = static_cast<char *>(workspace);
   BfsArgs a;
   a.row_ptr = row_ptr;
   a.edges = edges;
@@ -324,7 +832,9 @@ rdf2v_status launch_bfs_walks(const int32_t *row_ptr, const int32_t *edges, int6
   a.lens = len_out;
   a.counts = counts_out;
   a.status = status_dev;
-  a.workspace = static_cast<char *>(workspace);
+  a.queue_counts = reinterpret_cast<int32_t *>(ws);
+  for (int i = 0; i < 3; ++i) a.queue[i] = reinterpret_cast<int32_t *>(ws + 256 + i * align_up(size_t(num_roots) * 4, 256));
+  a.workspace = ws + queue_bytes(num_roots);
   a.slice_bytes = slice_bytes(num_entities);
   a.num_roots = num_roots;
   a.num_edges = num_edges;
@@ -332,8 +842,25 @@ rdf2v_status launch_bfs_walks(const int32_t *row_ptr, const int32_t *edges, int6
   a.num_predicates = num_predicates;
   a.depth = depth;
   a.max_walks = max_walks;
-  const int64_t grid = bfs_walks_grid(num_entities, num_roots);
-  bfs_walks_kernel<<<dim3(unsigned(grid)), dim3(kThreads), 0, stream>>>(a);
+  bfs_queue_reset_kernel<<<1, kWave, 0, stream>>>(a.queue_counts);
+  RDF2V_LAUNCH_CHECK();
+  // The first tier takes every root, one per workgroup (the hardware hands
+  // out roots as workgroups finish; at most 2^20 workgroups); a later tier
+  // runs a grid over its input queue, whose length only the device knows, and
+  // its workgroups past the end return at once.
+  const int first = bfs_first_tier(num_entities, num_edges, num_roots, depth);
+  for (int tier = first; tier < 3; ++tier) {
+    const int32_t *in_q = tier == first ? nullptr : a.queue[tier - 1];
+    const int32_t *in_c = tier == first ? nullptr : a.queue_counts + (tier - 1);
+    const int64_t grid = std::min<int64_t>(num_roots, tier == first ? int64_t(1) << 20 : 2048);
+    int32_t *taken = a.queue_counts + 3 + tier;
+    if (tier == 0) launch_tier<TinyTier>(a, in_q, in_c, taken, a.queue[0], a.queue_counts + 0, grid, stream);
+    else if (tier == 1) launch_tier<SmallTier>(a, in_q, in_c, taken, a.queue[1], a.queue_counts + 1, grid, stream);
+    else launch_tier<BigTier>(a, in_q, in_c, taken, a.queue[2], a.queue_counts + 2, grid, stream);
+    RDF2V_LAUNCH_CHECK();
+  }
+  const int64_t grid2 = bfs_walks_grid(num_entities, num_roots);
+  bfs_walks_kernel<<<dim3(unsigned(grid2)), dim3(kThreads), 0, stream>>>(a);
   RDF2V_LAUNCH_CHECK();
   return RDF2V_OK;
 }

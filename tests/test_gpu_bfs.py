@@ -50,7 +50,7 @@ def test_hand_graphs():
 
 
 @pytest.mark.parametrize("V,T,depth,seed", [(50, 150, 3, 0), (300, 1200, 4, 1), (2000, 6000, 6, 2),
-                                            (5000, 60_000, 2, 3), (40, 30, 10, 4)])
+                                            (5000, 60_000, 2, 3), (40, 30, 10, 4), (5000, 40_000, 3, 5)])
 def test_random_multigraphs(V, T, depth, seed):
     say(f"[bfs] random multigraph V={V} T={T} depth={depth}")
     P = 7
@@ -116,3 +116,87 @@ def test_out_of_range_root_is_flagged():
     torch.cuda.synchronize()
     assert int(st.item()) & rd.RDF2V_STATUS_ID_OUT_OF_RANGE
     assert cnt.cpu().tolist() == [1, 0, 1]
+
+
+@pytest.mark.parametrize("depth,max_walks", [(2, 256), (3, 1024), (3, 40)])
+def test_uniform_1m_every_start_sampled(depth, max_walks):
+    # the benchmark's launch: every start entity of the 1M-triple uniform graph
+    # in one call, trees of ~10^depth entities (up to ~2900 at depth 3); rows of
+    # 3000 sampled roots checked against the oracle
+    w = synth.WORKLOADS["uniform_1m"]
+    say(f"[bfs] uniform_1m every start, depth {depth}, max_walks {max_walks}")
+    s, p, o = synth.triples(w)
+    V, P = w.num_entities, w.num_predicates
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    roots = oracle.nonsink_starts(rp, V)
+    st = new_status()
+    tok, ln, cnt = rd.rdf2v_bfs_walks(csr, to_dev(roots), depth, max_walks, status=st)
+    torch.cuda.synchronize()
+    pick = np.sort(np.random.default_rng(depth * 7 + max_walks).choice(len(roots), 3000, replace=False))
+    ref_t, ref_l, ref_c, trunc = oracle.bfs_walks(rp, ed, V, P, roots[pick], depth, max_walks)
+    cnt = cnt.cpu().numpy()
+    assert np.array_equal(cnt[pick], ref_c)
+    tok = tok[torch.from_numpy(pick).to(device())].cpu().numpy()
+    ln = ln[torch.from_numpy(pick).to(device())].cpu().numpy()
+    for i in range(len(pick)):
+        k = ref_c[i]
+        assert np.array_equal(tok[i, :k], ref_t[i, :k]) and np.array_equal(ln[i, :k], ref_l[i, :k]), roots[pick[i]]
+    flags = int(st.item())
+    assert not flags & ~rd.RDF2V_STATUS_CAPACITY
+    if trunc > 0:
+        assert flags & rd.RDF2V_STATUS_CAPACITY
+    if flags & rd.RDF2V_STATUS_CAPACITY:
+        assert (cnt == max_walks).any()
+
+
+def test_trees_around_storage_limits():
+    # Roots whose trees have about 500 or 1000 entities above the depth limit,
+    # or about 1500 or 3000 in all: on both sides of the sizes where the kernels
+    # hand a root from the small on-chip tier to the big one and from there to
+    # the workspace pass; children reached twice, back edges into the tree and
+    # shuffled entity ids.
+    say("[bfs] trees around the on-chip storage limits")
+    V, P = 40_000, 3
+    rng = np.random.default_rng(5)
+    ids = rng.permutation(V).astype(np.int64)
+    nxt = [0]
+
+    def fresh(n):
+        out = ids[nxt[0]:nxt[0] + n]
+        nxt[0] += n
+        return out
+
+    trip = []
+    roots = []
+
+    def fan(root, kids, grand_per_kid):
+        for c in kids:
+            trip.append((root, int(rng.integers(P)), c))
+        trip.append((root, 0, kids[0]))                 # reached twice
+        for c in kids:
+            for g in fresh(grand_per_kid):
+                trip.append((c, int(rng.integers(P)), g))
+            if grand_per_kid:
+                trip.append((c, 1, root))               # back edge into the tree
+
+    for n_kids in (510, 511, 512, 1022, 1023, 1024, 1534, 1535, 1536, 3071, 3072):
+        r = fresh(1)[0]
+        roots.append(r)
+        fan(r, fresh(n_kids), 0)
+    for n_grand in (1533, 1534, 1535, 3069, 3070, 3071):
+        r = fresh(1)[0]
+        roots.append(r)
+        fan(r, fresh(1), n_grand)
+    r = fresh(1)[0]
+    roots.append(r)
+    fan(r, fresh(40), 75)                               # 1 + 40 + 3000 entities
+    t = np.array(trip, np.int64)
+    rng.shuffle(t)
+    s, p, o = (t[:, k].astype(np.int32) for k in range(3))
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    roots = np.array(roots + roots[:3], np.int32)
+    for depth in (1, 2, 3):
+        _compare(csr, rp, ed, V, P, roots, depth, 4000, f"limits depth {depth}")
+        _compare(csr, rp, ed, V, P, roots, depth, 1500, f"limits depth {depth} truncated")
