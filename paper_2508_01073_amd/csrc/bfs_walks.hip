@@ -186,7 +186,8 @@ __device__ __forceinline__ int32_t lanes_below(uint64_t b) {
 }
 
 // Exclusive prefix sum over the block (one value per thread) and its total.
-// Two barriers; scratch holds NT/64 ints.
+// One barrier; scratch holds NT/64 ints and must not be written again before
+// the next barrier (callers alternate between two scratch buffers).
 template <int NT>
 __device__ __forceinline__ int32_t block_scan(int32_t x, int32_t *scratch, int32_t &total) {
   constexpr int W = NT / kWave;
@@ -200,7 +201,6 @@ __device__ __forceinline__ int32_t block_scan(int32_t x, int32_t *scratch, int32
     if (lane == kWave - 1) scratch[w] = inc;
     __syncthreads();
     const int32_t waves = wave_inclusive_sum(lane < W ? scratch[lane] : 0);
-    __syncthreads();
     total = __builtin_amdgcn_readlane(waves, W - 1);
     return (w > 0 ? __builtin_amdgcn_readlane(waves, w - 1) : 0) + inc - x;
   }
@@ -208,7 +208,8 @@ __device__ __forceinline__ int32_t block_scan(int32_t x, int32_t *scratch, int32
 
 // Ranks, in pair order, the flagged pairs of a chunk whose round k holds pair
 // c0 + k*NT + threadIdx.x: rank[k] counts the flagged pairs before it in the
-// chunk; `total` is their number. Two barriers; cnt_s holds R * NT/64 ints.
+// chunk; `total` is their number. One barrier; cnt_s holds R * NT/64 ints and
+// is reused like the scratch of block_scan.
 template <int NT, int R>
 __device__ __forceinline__ void rank_chunk(uint32_t mask, int32_t (&rank)[R], int32_t &total, int32_t *cnt_s) {
   constexpr int W = NT / kWave;
@@ -225,7 +226,6 @@ __device__ __forceinline__ void rank_chunk(uint32_t mask, int32_t (&rank)[R], in
   }
   __syncthreads();
   const int32_t inc = wave_inclusive_sum(lane < R * W ? cnt_s[lane] : 0);
-  __syncthreads();
 #pragma unroll
   for (int k = 0; k < R; ++k) {
     const int32_t idx = k * W + w;
@@ -261,7 +261,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kWpe))) void
   static_assert(kCap < kSlots && kTreeCap <= kCap && kTreeCap <= 32767, "table and tree sizes");
   static_assert(kSlots % (4 * NT) == 0, "the table is cleared four slots per thread at a time");
   static_assert(R <= 32, "win masks are 32-bit");
-  __shared__ int32_t scan_scratch[R * (NT / kWave)];
+  __shared__ int32_t scan_scratch[2][R * (NT / kWave)];  // alternated between block-wide scans
   __shared__ __align__(16) int32_t h_key[kSlots];
   __shared__ __align__(16) uint32_t h_val[kSlots];
   __shared__ int32_t t_ent[kTreeCap];
@@ -314,6 +314,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kWpe))) void
   };
 
   int flags = 0;
+  int32_t phase = 0;
+  auto scratch = [&]() -> int32_t * { return scan_scratch[phase ^= 1]; };
   const int64_t n_in = in_queue != nullptr ? int64_t(*in_count) : a.num_roots;
   if (int64_t(blockIdx.x) >= n_in) return;  // uniform; an empty queue costs one load per workgroup
   for (int64_t k_in = blockIdx.x;; k_in += gridDim.x) {
@@ -409,7 +411,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kWpe))) void
       for (int32_t c0 = lb; c0 < le; c0 += NT) {
         const int32_t i = c0 + t;
         int32_t tot;
-        const int32_t ex = block_scan<NT>(i < le ? t_deg[i] : 0, scan_scratch, tot);
+        const int32_t ex = block_scan<NT>(i < le ? t_deg[i] : 0, scratch(), tot);
         if (i < le) dpre_s[i - lb] = carry + ex;
         carry += tot;
       }
@@ -417,6 +419,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kWpe))) void
       if (t == 0) dpre_s[nlev] = total;
       __syncthreads();
       const bool one_chunk = total <= kChunk;  // uniform: records stay in registers
+      const bool last = lev + 1 == a.depth;
       // Offers (tree members hold 0 and ignore them).
       bool full = false;
       int32_t inserted = 0;
@@ -443,7 +446,6 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kWpe))) void
       inserted = wave_sum(inserted);
       if (lane_id() == 0 && inserted > 0) atomicAdd(&used_s, inserted);
       __syncthreads();
-      const bool last = lev + 1 == a.depth;
       if (overflow_s || used_s > (last ? kCap : kTreeCap)) {  // uniform
         overflow = true;
         break;
@@ -462,7 +464,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kWpe))) void
         }
         {
           int32_t all;
-          (void)block_scan<NT>(n_wins, scan_scratch, all);
+          (void)block_scan<NT>(n_wins, scratch(), all);
           last_wins = all;
         }
         break;  // lb, le, nlev, total (and a one-chunk level's records) stay for the rows
@@ -471,31 +473,31 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kWpe))) void
       int32_t added = 0;
       for (int32_t c0 = 0; c0 < total; c0 += kChunk) {
         if (!one_chunk) load_chunk(c0);
-        int32_t rank[R], tot, row_lo[R], row_hi[R];
+        int32_t rank[R], tot, row_lo_k[R], row_hi_k[R];
         const uint32_t m = winners(c0, one_chunk);
 #pragma unroll
         for (int k = 0; k < R; ++k) {  // the new nodes' rows, in flight across the ranking
-          row_lo[k] = row_hi[k] = 0;
+          row_lo_k[k] = row_hi_k[k] = 0;
           if (m & (1u << k)) {
-            row_lo[k] = a.row_ptr[rec_k[k].y];
-            row_hi[k] = a.row_ptr[rec_k[k].y + 1];
+            row_lo_k[k] = a.row_ptr[rec_k[k].y];
+            row_hi_k[k] = a.row_ptr[rec_k[k].y + 1];
           }
         }
-        rank_chunk<NT, R>(m, rank, tot, scan_scratch);
+        rank_chunk<NT, R>(m, rank, tot, scratch());
 #pragma unroll
         for (int k = 0; k < R; ++k) {
           if (m & (1u << k)) {
             const int32_t pos = le + added + rank[k];  // < used_s <= kTreeCap
             const int32_t node = lb + node_k[k];
-            const bool ok = uint32_t(row_lo[k]) <= uint32_t(row_hi[k]) && uint32_t(row_hi[k]) <= E;
+            const bool ok = uint32_t(row_lo_k[k]) <= uint32_t(row_hi_k[k]) && uint32_t(row_hi_k[k]) <= E;
             if (!ok) flags |= RDF2V_STATUS_BAD_CSR;
             t_ent[pos] = rec_k[k].y;
             t_pred[pos] = rec_k[k].x;
             t_par[pos] = int16_t(node);
             t_lev[pos] = uint8_t(lev + 1);
             t_child[pos] = 0;
-            t_lo[pos] = row_lo[k];
-            t_deg[pos] = ok ? row_hi[k] - row_lo[k] : 0;
+            t_lo[pos] = row_lo_k[k];
+            t_deg[pos] = ok ? row_hi_k[k] - row_lo_k[k] : 0;
             t_child[node] = 1;
             h_val[slot_k[k]] = 0;
           }
@@ -526,7 +528,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kWpe))) void
       const int32_t i = c0 + t;
       const int32_t leaf = i < le ? int32_t(t_child[i] == 0) : 0;
       int32_t tot;
-      const int32_t ex = block_scan<NT>(leaf, scan_scratch, tot);
+      const int32_t ex = block_scan<NT>(leaf, scratch(), tot);
       const int32_t idx = leaves + ex;
       if (leaf && idx < a.max_walks) {
         const int32_t h = t_lev[i];
@@ -548,7 +550,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kWpe))) void
           m = winners(c0, false);
         }
         int32_t rank[R], tot;
-        rank_chunk<NT, R>(m, rank, tot, scan_scratch);
+        rank_chunk<NT, R>(m, rank, tot, scratch());
 #pragma unroll
         for (int k = 0; k < R; ++k) {
           const int32_t idx = leaves + added + rank[k];
