@@ -154,6 +154,7 @@ __device__ __forceinline__ uint64_t load_u64(const uint64_t *p) {
 }
 
 constexpr int kGroup = 1;           // inline words fetched together with the key
+constexpr int kBatchWords = 6;      // further inline words fetched together
 constexpr int32_t kDeferred = -2;   // parked in the id output: left to the general pass
 
 // What one look at a slot returns: the key, minpos and the first inline words,
@@ -213,13 +214,22 @@ __device__ __forceinline__ int32_t find_or_claim(Slot *__restrict__ table, int64
           differ = true;
       }
     }
+    // The other words in batches whose loads are all in flight together.
 #pragma unroll 1
-    for (int i = kGroup; i < nw; ++i) {
-      const uint64_t w = load_u64<__HIP_MEMORY_SCOPE_AGENT>(&sl->words[i]);
-      if ((w & ~kLow56) != kWritten)
-        unwritten = true;
-      else if (w != (word7_lds(lds, at, len, i) | kWritten))
-        differ = true;
+    for (int b = kGroup; b < nw; b += kBatchWords) {
+      uint64_t w[kBatchWords];
+#pragma unroll
+      for (int j = 0; j < kBatchWords; ++j)
+        w[j] = b + j < nw ? load_u64<__HIP_MEMORY_SCOPE_AGENT>(&sl->words[b + j]) : 0;
+#pragma unroll
+      for (int j = 0; j < kBatchWords; ++j) {
+        if (b + j < nw) {
+          if ((w[j] & ~kLow56) != kWritten)
+            unwritten = true;
+          else if (w[j] != (word7_lds(lds, at, len, b + j) | kWritten))
+            differ = true;
+        }
+      }
     }
     if (differ) continue;  // a different string
     if (unwritten) return kDeferred;
