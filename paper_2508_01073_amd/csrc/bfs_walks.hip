@@ -14,15 +14,16 @@
 // Leaves are then ranked in the order reached and the first max_walks become
 // rows root, V+p_1, v_1, ..., leaf.
 //
-// Three passes. Two LDS tiers run a root in LDS alone: the tree, the level's
-// degree prefix and an open-addressing hash table of the entities reached so
-// far (tree members and this level's offers). Every root goes to the small
-// tier first; a root whose tree outgrows a tier is abandoned there and queued
-// for the next one. The last pass, a persistent grid of workgroups that each
-// own a slice of the workspace (per-entity stamps and offers, the tree beyond
-// its first kTreeLds positions; about 36 bytes per entity), reruns the roots
-// neither tier could hold from scratch. All loops are bounded by the tree and
-// level sizes or the table size; there is no waiting on other workgroups.
+// Three LDS tiers run a root in one workgroup with all its state in LDS: the
+// tree above the depth limit, the level's degree prefix and an open-addressing
+// hash table of the entities reached so far (tree members and this level's
+// offers). Every root starts in one tier, picked from the expected tree size; a
+// root whose tree outgrows a tier is abandoned there and queued for the next.
+// The last pass, a persistent grid of workgroups that each own a slice of the
+// workspace (per-entity stamps and offers, the tree beyond its first kTreeLds
+// positions; about 36 bytes per entity), reruns the roots no tier could hold
+// from scratch. All loops are bounded by the tree and level sizes or the table
+// size; a workgroup never waits for another.
 
 #include <algorithm>
 
@@ -116,7 +117,7 @@ struct Tree {
 };
 
 // ---------------------------------------------------------------------------
-// First pass: one root at a time per workgroup, all state in LDS.
+// LDS tiers: one root at a time per workgroup, all state in LDS.
 
 // Three LDS tiers of growing capacity and LDS footprint: one wave per root
 // (about 6.3 KB of LDS, 24 workgroups per CU), 256 threads (about 25 KB, 6
@@ -581,7 +582,8 @@ __global__ void bfs_queue_reset_kernel(int32_t *queue_counts) {
 }
 
 // ---------------------------------------------------------------------------
-// Second pass: the queued roots, with per-workgroup slices of the workspace.
+// Workspace pass: the roots no tier could hold, with per-workgroup slices of
+// the workspace.
 
 __global__ __launch_bounds__(kThreads) void bfs_walks_kernel(const BfsArgs a) {
   __shared__ int32_t scan_scratch[kThreads / kWave];
@@ -807,7 +809,7 @@ int bfs_first_tier(int32_t num_entities, int64_t num_edges, int64_t num_roots, i
 }
 
 int64_t bfs_walks_grid(int32_t num_entities, int64_t num_roots) {
-  // Second pass: enough workgroups to fill the chip, at most ~4 GiB of slices.
+  // Workspace pass: enough workgroups to fill the chip, at most ~4 GiB of slices.
   const int64_t per = int64_t(slice_bytes(num_entities));
   int64_t g = std::max<int64_t>(1, (int64_t(1) << 32) / std::max<int64_t>(per, 1));
   g = std::min<int64_t>(g, 2048);
