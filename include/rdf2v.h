@@ -284,8 +284,8 @@ size_t rdf2v_bfs_walks_workspace_size(int32_t num_entities, int64_t num_roots);
  *   len_out      [num_roots][max_walks] int32, written like tokens_out.
  *   counts_out   [num_roots] int32: walks written per root. A root with more
  *                leaves than max_walks raises RDF2V_STATUS_CAPACITY.
- *   workspace    rdf2v_bfs_walks_workspace_size(V, num_roots) bytes (at most
- *                about 4 GiB), 256-byte aligned.
+ *   workspace    rdf2v_bfs_walks_workspace_size(V, num_roots) bytes (12 bytes
+ *                per root plus at most about 4 GiB), 256-byte aligned.
  */
 rdf2v_status rdf2v_bfs_walks(const rdf2v_csr *csr, const int32_t *roots, int64_t num_roots, int32_t depth,
                              int32_t max_walks, int32_t *tokens_out, int32_t *len_out, int32_t *counts_out,

@@ -200,3 +200,19 @@ def test_trees_around_storage_limits():
     for depth in (1, 2, 3):
         _compare(csr, rp, ed, V, P, roots, depth, 4000, f"limits depth {depth}")
         _compare(csr, rp, ed, V, P, roots, depth, 1500, f"limits depth {depth} truncated")
+
+
+def test_inconsistent_csr_is_flagged_not_read():
+    # row_ptr decreasing at entity 1, past num_edges at entity 2 and 3: every row
+    # is checked before its records are read, so BFS only raises the status bit
+    say("[bfs] inconsistent CSR")
+    dev = device()
+    row_ptr = torch.tensor([0, 3, 1, 50, 4], dtype=torch.int32, device=dev)
+    edges = torch.tensor([[0, 1], [0, 2], [0, 1], [0, 3]], dtype=torch.int32, device=dev)
+    csr = rd.Csr(row_ptr, edges, 4, 1)
+    for roots in ([0], [1], [2, 3], [0, 1, 2, 3] * 50):
+        st = new_status()
+        tok, ln, cnt = rd.rdf2v_bfs_walks(csr, to_dev(roots), 3, 8, status=st)
+        torch.cuda.synchronize()
+        assert int(st.item()) & rd.RDF2V_STATUS_BAD_CSR, roots
+        assert bool((cnt >= 0).all()) and bool((cnt <= 8).all())
