@@ -108,20 +108,20 @@ __global__ __launch_bounds__(kThreads) void pair_offsets_kernel(const int32_t *_
 
 // One thread per (walk, center); walks_per_block = kBlock / width walks per
 // block, whose rows are contiguous in the input and whose pairs form one
-// contiguous output range. When that range fits in LDS (kStagePairs), the block
-// first copies its rows to LDS with one coalesced load, the threads place their
-// pairs in LDS, and the block streams the range out with consecutive,
-// non-temporal 16-byte stores; otherwise each thread reads its row from global
-// memory and writes its pairs directly. kStagePairs is the LDS stage, in pairs.
+// contiguous output range. With kStage, the block first copies its rows to LDS
+// with one coalesced load, the threads place their pairs in an LDS stage sized
+// at launch to the block's most pairs (dynamic LDS), and the block streams the
+// range out with consecutive, non-temporal 16-byte stores; otherwise each
+// thread reads its row from global memory and writes its pairs directly.
 
-template <bool kStage, int kBlock, int kStagePairs>
+template <bool kStage, int kBlock>
 __global__ __launch_bounds__(kBlock) void pair_emit_kernel(const int32_t *__restrict__ tokens,
                                                              const int32_t *__restrict__ len, int64_t n,
                                                              int32_t width, int32_t window,
                                                              const int64_t *__restrict__ offsets,
                                                              int2 *__restrict__ pairs, int64_t capacity,
                                                              int32_t *status) {
-  __shared__ int2 stage[kStage ? kStagePairs : 1];
+  extern __shared__ int2 stage[];                // kStage: the block's pairs
   __shared__ int32_t rows[kStage ? kBlock : 1];  // the block's walk rows, walks_per_block * width tokens
   const int walks_per_block = kBlock / width;
   const int t = threadIdx.x;
@@ -198,6 +198,8 @@ __global__ __launch_bounds__(kBlock) void pair_emit_kernel(const int32_t *__rest
     atomicOr(status, (full ? RDF2V_STATUS_CAPACITY : 0) | (bad ? RDF2V_STATUS_BAD_LENGTH : 0));
 }
 
+constexpr size_t kMaxStageBytes = 32 << 10;
+
 // Most pairs one walk of this width can give.
 inline int64_t max_walk_pairs(int64_t width, int64_t window) {
   const int64_t m = std::min(window, width - 1);
@@ -234,22 +236,27 @@ rdf2v_status launch_skipgram_pairs(const int32_t *tokens, const int32_t *len, in
   RDF2V_LAUNCH_CHECK();
   if (capacity > 0) {
     int2 *out = reinterpret_cast<int2 *>(pairs_out);
-    // The largest block whose pairs still fit the LDS stage: more walks per
-    // block for short windows, so that each block streams a longer range.
+    // Blocks of 256 threads when their pairs fit a stage of at most
+    // kMaxStageBytes, else of 128 or 64: several small blocks per CU keep the
+    // write stream going while others load rows and place pairs (measured:
+    // 256 threads with a ~17 KB stage beat 512 and 1024 with 33-67 KB).
     const int64_t per_walk = max_walk_pairs(width, window);
-    auto fits = [&](int block, int stage) { return width <= block && per_walk * (block / width) <= stage; };
-    auto launch = [&](auto kernel, int block) -> rdf2v_status {
+    auto stage_bytes = [&](int block) { return size_t(per_walk * (block / width)) * sizeof(int2); };
+    auto launch = [&](auto kernel, int block, size_t lds) -> rdf2v_status {
       const int64_t blocks = ceil_div(num_walks, block / width);
       if (blocks >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
-      kernel<<<dim3(unsigned(blocks)), dim3(block), 0, stream>>>(tokens, len, num_walks, width, window, offsets,
-                                                                 out, capacity, status_dev);
+      kernel<<<dim3(unsigned(blocks)), dim3(block), lds, stream>>>(tokens, len, num_walks, width, window, offsets,
+                                                                   out, capacity, status_dev);
       RDF2V_LAUNCH_CHECK();
       return RDF2V_OK;
     };
-    if (fits(1024, 4096)) return launch(pair_emit_kernel<true, 1024, 4096>, 1024);
-    if (fits(512, 5120)) return launch(pair_emit_kernel<true, 512, 5120>, 512);
-    if (fits(kThreads, 4096)) return launch(pair_emit_kernel<true, kThreads, 4096>, kThreads);
-    return launch(pair_emit_kernel<false, kThreads, 1>, kThreads);
+    if (width <= 256 && stage_bytes(256) <= kMaxStageBytes)
+      return launch(pair_emit_kernel<true, 256>, 256, stage_bytes(256));
+    if (width <= 128 && stage_bytes(128) <= kMaxStageBytes)
+      return launch(pair_emit_kernel<true, 128>, 128, stage_bytes(128));
+    if (width <= 64 && stage_bytes(64) <= kMaxStageBytes)
+      return launch(pair_emit_kernel<true, 64>, 64, stage_bytes(64));
+    return launch(pair_emit_kernel<false, kThreads>, kThreads, 0);
   }
   return RDF2V_OK;
 }
