@@ -10,7 +10,8 @@
 //      hash, length and tokens (equal hashes are always confirmed token by
 //      token, so collisions cannot drop a walk). Keep flags go to global
 //      memory, the block's kept count to a partial sum.
-//   2. keep_partials_kernel: exclusive scan of the block counts.
+//   2. an exclusive scan of the block counts (tiles scanned in parallel, then
+//      the tile totals, then each tile's prefix added).
 //   3. group_compact_kernel: the block stages its rows again, scans its keep
 //      flags and writes its kept rows as one contiguous range.
 // Other shapes use the general path: a hash per row, a group scan over the
@@ -108,7 +109,38 @@ __global__ __launch_bounds__(kThreads) void keep_count_kernel(const int32_t *__r
   if (threadIdx.x == 0) partials[blockIdx.x] = total;
 }
 
-// One block: exclusive scan of the nb block counts in place, kItems consecutive
+// Exclusive scan of the nb block counts, in place, in three launches:
+// tile_scan_kernel scans each tile of kTile counts and writes the tile's total
+// to tile_sums; keep_partials_kernel (one block) scans the tile totals; and
+// tile_add_kernel adds each tile's prefix to its counts.
+__global__ __launch_bounds__(kThreads) void tile_scan_kernel(int64_t *partials, int64_t nb,
+                                                             int64_t *tile_sums) {
+  __shared__ int64_t scratch[kThreads / kWave];
+  const int64_t first = int64_t(blockIdx.x) * kTile + int64_t(threadIdx.x) * kItems;
+  int64_t v[kItems];
+  int64_t s = 0;
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    v[i] = first + i < nb ? partials[first + i] : 0;
+    s += v[i];
+  }
+  int64_t tot;
+  int64_t ex = block_exclusive_scan<kThreads, int64_t>(s, scratch, tot);
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    if (first + i < nb) partials[first + i] = ex;
+    ex += v[i];
+  }
+  if (threadIdx.x == 0) tile_sums[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(kThreads) void tile_add_kernel(int64_t *partials, int64_t nb,
+                                                            const int64_t *tile_sums) {
+  const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  if (i < nb) partials[i] += tile_sums[i / kTile];
+}
+
+// One block: exclusive scan of the nb counts in place, kItems consecutive
 // counts per thread per round; the total goes to partials[nb] and *total_out.
 __global__ __launch_bounds__(kThreads) void keep_partials_kernel(int64_t *partials, int64_t nb,
                                                                  int64_t *total_out) {
@@ -179,6 +211,24 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const int32_t *__rest
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Exclusive scan of nb counts in place, total to *total_out; tile_sums holds
+// ceil(nb / kTile) + 1 entries, counts nb + 1.
+rdf2v_status scan_counts(int64_t *counts, int64_t nb, int64_t *tile_sums, int64_t *total_out,
+                         hipStream_t stream) {
+  const int64_t tiles = ceil_div(nb, kTile);
+  if (tiles > 1) {
+    tile_scan_kernel<<<dim3(unsigned(tiles)), dim3(kThreads), 0, stream>>>(counts, nb, tile_sums);
+    RDF2V_LAUNCH_CHECK();
+    keep_partials_kernel<<<dim3(1), dim3(kThreads), 0, stream>>>(tile_sums, tiles, total_out);
+    RDF2V_LAUNCH_CHECK();
+    tile_add_kernel<<<dim3(unsigned(ceil_div(nb, kThreads))), dim3(kThreads), 0, stream>>>(counts, nb, tile_sums);
+  } else {
+    keep_partials_kernel<<<dim3(1), dim3(kThreads), 0, stream>>>(counts, nb, total_out);
+  }
+  RDF2V_LAUNCH_CHECK();
+  return RDF2V_OK;
+}
+
 // ---------------------------------------------------------------------------
 // Main path: blocks of whole groups.
 // ---------------------------------------------------------------------------
@@ -213,34 +263,62 @@ __global__ __launch_bounds__(NT) void group_keep_kernel(const int32_t *__restric
                                                               int32_t width, int32_t group, int32_t rows_per_block,
                                                               uint8_t *__restrict__ keep,
                                                               int64_t *__restrict__ partials, int32_t *status) {
+  constexpr int kSlots = 2 * NT;      // open-addressing table of (group, hash) keys
+  constexpr uint64_t kNoKey = ~uint64_t(0);
   extern __shared__ int32_t tile[];  // rows_per_block * width ints
   __shared__ uint64_t hashes[NT];
   __shared__ int32_t lens[NT];
   __shared__ int64_t scratch[NT / kWave];
+  __shared__ uint64_t tab_key[kSlots];
+  __shared__ int32_t tab_first[kSlots];  // smallest row of the block with the slot's key
+  const int t = threadIdx.x;
+  for (int i = t; i < kSlots; i += NT) {
+    tab_key[i] = kNoKey;
+    tab_first[i] = INT32_MAX;
+  }
   const int64_t r0 = int64_t(blockIdx.x) * rows_per_block;
   const int32_t rows = int32_t(min(int64_t(rows_per_block), n - r0));
   stage_ints<NT>(tile, tokens + r0 * width, rows * width);
   __syncthreads();
-  const int t = threadIdx.x;
   int bad = 0;
-  int32_t L = 0;
+  int32_t L = 0, slot = 0;
   if (t < rows) {
     L = clamp_len(len[r0 + t], width, bad);
-    hashes[t] = row_hash(tile + t * width, L);
+    const uint64_t h = row_hash(tile + t * width, L);
+    hashes[t] = h;
     lens[t] = L;
+    // Key: the hash with the row's group mixed in (two groups' keys may still
+    // meet: rows are always compared before one is dropped).
+    uint64_t key = h ^ (uint64_t(t / group + 1) * 0x9e3779b97f4a7c15ull);
+    if (key == kNoKey) key = kNoKey - 1;
+    slot = int32_t((key ^ (key >> 29)) & uint64_t(kSlots - 1));
+    for (int n_probe = 0; n_probe < kSlots; ++n_probe) {  // the table has more slots than rows
+      const uint64_t cur = atomicCAS(reinterpret_cast<unsigned long long *>(tab_key + slot),
+                                     static_cast<unsigned long long>(kNoKey), static_cast<unsigned long long>(key));
+      if (cur == kNoKey || cur == key) break;
+      slot = (slot + 1) & (kSlots - 1);
+    }
+    atomicMin(tab_first + slot, t);
   }
   __syncthreads();
   int32_t k = 0;
   if (t < rows) {
     const uint64_t h = hashes[t];
     const int32_t *row = tile + t * width;
-    bool dup = false;
-    for (int32_t q = t / group * group; q < t && !dup; ++q) {
-      if (hashes[q] != h || lens[q] != L) continue;
+    auto same_row = [&](int32_t q) {
+      if (hashes[q] != h || lens[q] != L) return false;
       const int32_t *other = tile + q * width;
-      bool same = true;
-      for (int32_t j = 0; j < L && same; ++j) same = other[j] == row[j];
-      dup = same;
+      for (int32_t j = 0; j < L; ++j)
+        if (other[j] != row[j]) return false;
+      return true;
+    };
+    // The first row with this key is usually the first occurrence of this
+    // walk; when it is not (a key collision), scan the group's earlier rows.
+    const int32_t first = tab_first[slot];
+    bool dup = false;
+    if (first != t) {
+      dup = first / group == t / group && same_row(first);
+      for (int32_t q = t / group * group; q < t && !dup; ++q) dup = same_row(q);
     }
     k = dup ? 0 : 1;
     keep[r0 + t] = uint8_t(k);
@@ -302,6 +380,9 @@ rdf2v_status launch_unique_walks(const int32_t *tokens, const int32_t *len, int6
   // 8 B per block + 1), the keep flags after them.
   int64_t *block_counts = reinterpret_cast<int64_t *>(ws);
   uint8_t *keep_flags = reinterpret_cast<uint8_t *>(ws + align_up(size_t(num_walks) * 8, 256));
+  // the scan's tile sums where the general path keeps its partials
+  int64_t *tile_sums = reinterpret_cast<int64_t *>(ws + align_up(size_t(num_walks) * 8, 256) +
+                                                   align_up(size_t(num_walks) * 4, 256));
   auto main_path = [&](auto keep_kernel, auto compact_kernel, int nt) -> rdf2v_status {
     const int32_t rows_per_block = (nt / group) * group;
     const size_t tile_bytes = size_t(rows_per_block) * width * sizeof(int32_t);
@@ -313,8 +394,8 @@ rdf2v_status launch_unique_walks(const int32_t *tokens, const int32_t *len, int6
                                                                         status_dev);
       RDF2V_LAUNCH_CHECK();
     }
-    keep_partials_kernel<<<dim3(1), dim3(kThreads), 0, stream>>>(block_counts, nb, count_out);
-    RDF2V_LAUNCH_CHECK();
+    const rdf2v_status st = scan_counts(block_counts, nb, tile_sums, count_out, stream);
+    if (st != RDF2V_OK) return st;
     if (nb > 0) {
       compact_kernel<<<dim3(unsigned(nb)), dim3(nt), tile_bytes, stream>>>(tokens, len, num_walks, width,
                                                                            rows_per_block, keep_flags, block_counts,
@@ -346,8 +427,9 @@ rdf2v_status launch_unique_walks(const int32_t *tokens, const int32_t *len, int6
     keep_count_kernel<<<dim3(unsigned(nb)), dim3(kThreads), 0, stream>>>(keep, num_walks, partials);
     RDF2V_LAUNCH_CHECK();
   }
-  keep_partials_kernel<<<dim3(1), dim3(kThreads), 0, stream>>>(partials, nb, count_out);
-  RDF2V_LAUNCH_CHECK();
+  // the hashes are no longer needed: their space holds the tile sums of the scan
+  const rdf2v_status st = scan_counts(partials, nb, reinterpret_cast<int64_t *>(ws), count_out, stream);
+  if (st != RDF2V_OK) return st;
   if (num_walks > 0) {
     compact_kernel<<<dim3(unsigned(nb)), dim3(kThreads), 0, stream>>>(tokens, len, num_walks, width, keep,
                                                                      partials, tokens_out, len_out);

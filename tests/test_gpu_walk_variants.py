@@ -128,3 +128,21 @@ def test_unique_walks_tiny_uniform_corpus():
     got_t, got_l = _gpu_unique(tok, ln, w.walks_per_node)
     assert_rows_equal(got_t, got_l, ref_t, ref_l, "tiny_uniform unique")
     assert ref_t.shape[0] < tok.shape[0]
+
+
+def _random_rows(rng, n, width, alphabet):
+    ln = (2 * rng.integers(0, (width + 1) // 2, n) + 1).astype(np.int32)
+    tok = rng.integers(0, alphabet, (n, width)).astype(np.int32)
+    tok[np.arange(width)[None, :] >= ln[:, None]] = -1
+    return tok, ln
+
+
+@pytest.mark.parametrize("n,width,group", [(1_200_007, 9, 7), (17_000_003, 3, 1025)])
+def test_unique_walks_many_block_counts(n, width, group):
+    # enough blocks (whole-group blocks of <= 256 rows; 4096-row tiles on the
+    # general path) that their kept counts are scanned in several tiles
+    say(f"[unique] {n} rows, width {width}, group {group}")
+    tok, ln = _random_rows(np.random.default_rng(n), n, width, 3)
+    ref_t, ref_l = oracle.unique_walks(tok, ln, group)
+    got_t, got_l = _gpu_unique(tok, ln, group)
+    assert_rows_equal(got_t, got_l, ref_t, ref_l, f"{n} rows group {group}")
