@@ -3,6 +3,11 @@
 // plain streaming copy. It explains the walk kernel's ceiling: a walk hop is
 // one dependent random read that almost always misses L2.
 //
+// A second table separates the possible limits: the same cache lines spread
+// over a larger address range (more pages, same cache footprint) tests TLB
+// reach; several independent chains per lane and fewer lanes test whether the
+// rate is set by the number of reads in flight.
+//
 // Every index is reduced modulo the table size, so all accesses are in bounds.
 // Fine-grained and uncached allocations are never freed (the process ends).
 #include <hip/hip_runtime.h>
@@ -59,6 +64,47 @@ __global__ __launch_bounds__(256) void chase(const v4i *__restrict__ t, uint64_t
   out[lane] = acc + idx;
 }
 
+// Physical record of logical record i when the table's 128-byte lines (8
+// records) are spread by a power-of-two factor g: line L lands at a pseudo-random
+// line inside [L*g, L*g + g), so cache sets and channels stay uniformly used.
+// The largest index is n*g - 1 for n a multiple of 8.
+__device__ __forceinline__ uint64_t spread_index(uint32_t i, uint32_t g) {
+  const uint64_t line = i >> 3;
+  return ((line * g + (mix(uint32_t(line) ^ 0x5bd1e995u) & (g - 1))) << 3) | (i & 7u);
+}
+
+__global__ void fill_spread(v4i *t, uint32_t n, uint32_t g) {
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+    const uint32_t h = mix(i * 2654435761u + 12345u);
+    t[spread_index(i, g)] = v4i{int32_t((uint64_t(h) * n) >> 32), int32_t(h), int32_t(i), 0};
+  }
+}
+
+// K independent chains per lane over a spread table, 16-byte reads.
+template <int K>
+__global__ __launch_bounds__(256) void chase_chains(const v4i *__restrict__ t, uint32_t n, uint32_t g, int steps,
+                                                    uint32_t *out) {
+  const uint32_t lane = blockIdx.x * 256 + threadIdx.x;
+  uint32_t idx[K];
+  uint32_t acc = 0;
+#pragma unroll
+  for (int k = 0; k < K; ++k) idx[k] = uint32_t((uint64_t(mix(lane * K + k)) * n) >> 32);
+  for (int s = 0; s < steps; ++s) {
+    v4i v[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) v[k] = t[spread_index(idx[k], g)];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      idx[k] = uint32_t(v[k].x);
+      acc += uint32_t(v[k].y + v[k].z);
+    }
+  }
+  uint32_t r = acc;
+#pragma unroll
+  for (int k = 0; k < K; ++k) r += idx[k];
+  out[lane] = r;
+}
+
 __global__ void copy16(const v4i *a, v4i *b, uint64_t n) {
   for (uint64_t i = blockIdx.x * uint64_t(blockDim.x) + threadIdx.x; i < n; i += uint64_t(gridDim.x) * blockDim.x)
     b[i] = a[i];
@@ -84,6 +130,27 @@ int run(const v4i *t, uint64_t n, uint32_t *out, const char *what, hipEvent_t a,
   const double g = double(lanes) * steps / (ms * 1e-3);
   std::printf("| %-34s | %10.1f | %8.3f | %7.1f | %llu |\n", what, n * 16.0 / 1e6, ms, g / 1e9,
               (unsigned long long)sum);
+  return 0;
+}
+
+template <int K>
+int run_chains(const v4i *t, uint32_t n, uint32_t g, uint32_t lanes, uint32_t *out, hipEvent_t a, hipEvent_t b) {
+  const int steps = 32;
+  chase_chains<K><<<lanes / 256, 256>>>(t, n, g, steps, out);
+  CK(hipDeviceSynchronize());
+  CK(hipEventRecord(a));
+  chase_chains<K><<<lanes / 256, 256>>>(t, n, g, steps, out);
+  CK(hipEventRecord(b));
+  CK(hipEventSynchronize(b));
+  float ms = 0;
+  CK(hipEventElapsedTime(&ms, a, b));
+  CK(hipMemcpy(host_out, out, lanes * sizeof(uint32_t), hipMemcpyDeviceToHost));
+  uint64_t sum = 0;
+  for (uint32_t i = 0; i < lanes; ++i) sum += host_out[i];
+  const double g_per_s = double(lanes) * steps * K / (ms * 1e-3);
+  std::printf("| %10.1f | %6u | %10.1f | %9u | %6d | %8.3f | %7.1f | %llu |\n", n * 16.0 / 1e6, g,
+              n * 16.0 * g / 1e6, lanes, K, ms, g_per_s / 1e9, (unsigned long long)sum);
+  std::fflush(stdout);
   return 0;
 }
 
@@ -139,5 +206,33 @@ int main() {
   fill<<<4096, 256>>>(tu, n);
   CK(hipDeviceSynchronize());
   if (run<0>(tu, n, out, "8 B, uncached memory", a, b)) return 1;
+
+  std::printf("\n16-byte dependent reads: working set (lines MB), spread factor (span MB = lines MB x spread),\n"
+              "lanes and independent chains per lane; 32 reads per chain\n\n");
+  std::printf("| lines MB | spread | span MB | lanes | chains | ms | G reads/s | checksum |\n");
+  std::printf("|---|---|---|---|---|---|---|---|\n");
+  struct Case {
+    uint32_t n, g;
+  };
+  const Case cases[] = {
+      {1u << 18, 1},  {1u << 18, 16}, {1u << 18, 256}, {1u << 20, 1},  {1u << 20, 4},  {1u << 20, 16},
+      {1u << 20, 64}, {1u << 20, 256}, {1u << 21, 1},  {1u << 21, 64}, {1u << 22, 1},  {1u << 22, 32},
+      {6u << 20, 1},  {10u << 20, 1}, {1u << 24, 1},   {1u << 28, 1},
+  };
+  const uint32_t full = 1u << 21;
+  for (const Case &c : cases) {
+    if (uint64_t(c.n) * c.g > maxn) continue;  // every index stays inside the 4 GiB table
+    fill_spread<<<4096, 256>>>(t, c.n, c.g);
+    CK(hipDeviceSynchronize());
+    if (run_chains<1>(t, c.n, c.g, full, out, a, b)) return 1;
+    if (c.g == 1 && (c.n == (10u << 20) || c.n == (1u << 28))) {
+      if (run_chains<2>(t, c.n, c.g, full, out, a, b)) return 1;
+      if (run_chains<4>(t, c.n, c.g, full, out, a, b)) return 1;
+      if (run_chains<1>(t, c.n, c.g, full / 4, out, a, b)) return 1;
+      if (run_chains<1>(t, c.n, c.g, full / 8, out, a, b)) return 1;
+      if (run_chains<1>(t, c.n, c.g, full / 16, out, a, b)) return 1;
+      if (run_chains<4>(t, c.n, c.g, full / 16, out, a, b)) return 1;
+    }
+  }
   return 0;
 }
