@@ -157,6 +157,21 @@ constexpr int kGroup = 1;           // inline words fetched together with the ke
 constexpr int kBatchWords = 6;      // further inline words fetched together
 constexpr int32_t kDeferred = -2;   // parked in the id output: left to the general pass
 
+// The fast pass reads slots through the caches (wavefront-scope loads, which
+// may hit a line the CU's L1 or the XCD's L2 fetched earlier) instead of at
+// agent scope (loads marked device-coherent, which made the fast pass about
+// 20% slower on the 20M-triple power-law graph). A cached value can be
+// stale but never wrong, because every field moves one way during the pass:
+// the key goes from empty to its final value once (by compare-and-swap), each
+// inline word from 0 to its final value once, and minpos only decreases. So a
+// stale key reads as empty and the compare-and-swap then returns the real one;
+// a stale word reads as not written and the occurrence is left to the general
+// pass, which reads at agent scope; a stale minpos is larger than the real one
+// and at worst costs an atomicMin that changes nothing. Values left by earlier
+// kernels (a previous call on the same table) are not visible: each kernel
+// starts after the table was reset by the previous one.
+constexpr int kFastScope = __HIP_MEMORY_SCOPE_WAVEFRONT;
+
 // What one look at a slot returns: the key, minpos and the first inline words,
 // all loaded at once (one round trip; they share the slot's line).
 struct SlotView {
@@ -167,10 +182,10 @@ struct SlotView {
 
 __device__ __forceinline__ SlotView view_slot(const Slot *sl, int nw) {
   SlotView v;
-  v.key = load_u64<__HIP_MEMORY_SCOPE_AGENT>(&sl->key);
-  v.minpos = __hip_atomic_load(&sl->minpos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  v.key = load_u64<kFastScope>(&sl->key);
+  v.minpos = __hip_atomic_load(&sl->minpos, __ATOMIC_RELAXED, kFastScope);
 #pragma unroll
-  for (int i = 0; i < kGroup; ++i) v.w[i] = i < nw ? load_u64<__HIP_MEMORY_SCOPE_AGENT>(&sl->words[i]) : 0;
+  for (int i = 0; i < kGroup; ++i) v.w[i] = i < nw ? load_u64<kFastScope>(&sl->words[i]) : 0;
   return v;
 }
 
@@ -220,7 +235,7 @@ __device__ __forceinline__ int32_t find_or_claim(Slot *__restrict__ table, int64
       uint64_t w[kBatchWords];
 #pragma unroll
       for (int j = 0; j < kBatchWords; ++j)
-        w[j] = b + j < nw ? load_u64<__HIP_MEMORY_SCOPE_AGENT>(&sl->words[b + j]) : 0;
+        w[j] = b + j < nw ? load_u64<kFastScope>(&sl->words[b + j]) : 0;
 #pragma unroll
       for (int j = 0; j < kBatchWords; ++j) {
         if (b + j < nw) {
