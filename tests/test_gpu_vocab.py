@@ -225,6 +225,32 @@ def test_deterministic_across_calls_and_streams():
     assert a[3] == b[3]
 
 
+def test_reused_workspace_across_vocabularies():
+    # One workspace serves two calls over the same strings in opposite triple orders, so every
+    # string gets another id and another first occurrence in the second call. Each call resets the
+    # table; a slot the first call claimed must read as empty again in the second, or its string
+    # would be found there and never claimed (the fast pass reads slots through the caches).
+    say("[vocab] reused workspace")
+    w = synth.WORKLOADS["uniform_1m"]
+    S, P, O = synth.triples(w)
+    T = S.shape[0]
+    ws = torch.empty(rd.rdf2v_build_vocabulary_workspace_size(T, w.num_entities, w.num_predicates),
+                     dtype=torch.uint8, device=device())
+    for order in ("forward", "reversed"):
+        if order == "reversed":
+            S, P, O = S[::-1].copy(), P[::-1].copy(), O[::-1].copy()
+        cols = synth.string_triples(S, P, O, w.num_entities, w.num_predicates)
+        ref = oracle.build_vocabulary(cols[0][0], cols[0][1], cols[1][0], cols[1][1], cols[2][0], cols[2][1])
+        st = new_status()
+        s, p, o, counts = rd.rdf2v_build_vocabulary(*[_dev_col(c) for c in cols], w.num_entities,
+                                                    w.num_predicates, workspace=ws, status=st)
+        torch.cuda.synchronize()
+        assert int(st.item()) == 0
+        assert counts.cpu().numpy().tolist() == [ref[3], ref[4]]
+        for got, exp in ((s, ref[0]), (p, ref[1]), (o, ref[2])):
+            assert np.array_equal(got.cpu().numpy(), exp), order
+
+
 def test_string_pipeline_end_to_end():
     # strings -> ids on the GPU -> CSR -> walks equals the oracle pipeline from the same strings
     say("[vocab] end to end")
