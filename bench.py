@@ -3,8 +3,9 @@
 
 One step is one pass of the whole path over inputs already resident in HBM:
 rdf2v_build_csr (triples -> CSR), rdf2v_build_walk_edges (16-byte walk
-records), rdf2v_nonsink_starts (start set) and rdf2v_random_walks (every walk
-of every start entity, one launch). The default
+records, when rdf2v_walk_edges_recommended says they pay for this graph size),
+rdf2v_nonsink_starts (start set) and rdf2v_random_walks (every walk of every
+start entity, one launch). The default
 workload is the power-law graph with 1M entities, 200 predicates and 20M
 triples, depth 8, 50 walks per start entity (about 48.9M walks).
 
@@ -298,6 +299,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="powerlaw_20m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--walk-records", choices=["auto", "on", "off"], default="auto",
+                    help="build 16-byte walk records in the step: as rdf2v_walk_edges_recommended "
+                         "advises for the graph size (auto), always, or never")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--tokens", choices=["triples", "entities", "properties"], default="triples",
                     help="walk rows: entity/predicate triples (default), entity walks or property walks")
@@ -345,7 +349,8 @@ def main() -> int:
     row_ptr = torch.empty(V + 1, dtype=torch.int32, device=dev)
     edges = torch.empty((T, 2), dtype=torch.int32, device=dev)
     ws_build = torch.empty(max(rd.rdf2v_build_csr_workspace_size(T, V), 1), dtype=torch.uint8, device=dev)
-    walk_edges = torch.empty((T, 4), dtype=torch.int32, device=dev)
+    use_records = {"auto": rd.rdf2v_walk_edges_recommended(V, T), "on": True, "off": False}[args.walk_records]
+    walk_edges = torch.empty((T, 4), dtype=torch.int32, device=dev) if use_records else None
     ws_starts = torch.empty(rd.rdf2v_nonsink_starts_workspace_size(V), dtype=torch.uint8, device=dev)
     starts = torch.empty(V, dtype=torch.int32, device=dev)
     count = torch.empty(1, dtype=torch.int64, device=dev)
@@ -383,7 +388,8 @@ def main() -> int:
         e0.record(stream)
         csr = rd.rdf2v_build_csr(subj, pred, obj, V, P, workspace=ws_build, status=status,
                                  row_ptr=row_ptr, edges=edges, stream=stream)
-        csr = rd.rdf2v_build_walk_edges(csr, out=walk_edges, status=status, stream=stream)
+        if use_records:
+            csr = rd.rdf2v_build_walk_edges(csr, out=walk_edges, status=status, stream=stream)
         e1.record(stream)
         st, cnt = rd.rdf2v_nonsink_starts(csr, workspace=ws_starts, starts=starts, count=count,
                                           stream=stream, sync=False)
@@ -449,6 +455,7 @@ def main() -> int:
             "workload": w.name, "num_entities": V, "num_predicates": P, "num_triples": T,
             "graph": w.kind, "depth": d, "walks_per_node": wpn, "num_start": n_start,
             "num_walks": n_walks, "seed": 42, "batch_walks": batch_cap if launches > 1 else None,
+            "walk_records": use_records,
         },
         "roofline": {
             "kernel": "random_walk_kernel",

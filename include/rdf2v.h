@@ -128,6 +128,22 @@ rdf2v_status rdf2v_build_csr(const int32_t *subj, const int32_t *pred, const int
 rdf2v_status rdf2v_build_walk_edges(const rdf2v_csr *csr, int32_t *walk_edges_out,
                                     int32_t *status_dev, void *stream);
 
+/*
+ * Whether walk records are expected to make rdf2v_random_walks faster on a
+ * CSR of this size than row_ptr and edges read directly (the walks are
+ * identical either way). Pure host function; 1 = build them, 0 = do not.
+ *
+ * Without records a hop reads the current entity's row bounds and then one
+ * 8-byte record; with them it reads one 16-byte record from a table twice as
+ * large. While row_ptr (4 * (num_entities + 1) bytes) stays resident in each
+ * XCD's 4 MB L2 the bound read is a cache hit and the smaller record table
+ * wins; beyond that every hop pays a second cache miss. Measured crossover on
+ * gfx950 (uniform and power-law graphs, mean out-degree 20, depth 8):
+ * row_ptr between 1.2 and 2.0 MB, so this returns 1 when row_ptr is larger
+ * than 1.5 MiB and num_edges > 0. Negative sizes return 0.
+ */
+int32_t rdf2v_walk_edges_recommended(int32_t num_entities, int64_t num_edges);
+
 /* Bytes of device workspace rdf2v_nonsink_starts needs. Pure host function. */
 size_t rdf2v_nonsink_starts_workspace_size(int32_t num_entities);
 

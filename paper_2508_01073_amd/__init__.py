@@ -25,6 +25,7 @@ __all__ = [
     "Csr", "Rdf2vError", "RDF2V_MAX_DEPTH", "RDF2V_STATUS_ID_OUT_OF_RANGE", "RDF2V_STATUS_BAD_CSR",
     "RDF2V_TOKENS_TRIPLES", "RDF2V_TOKENS_ENTITIES", "RDF2V_TOKENS_PROPERTIES",
     "rdf2v_build_csr_workspace_size", "rdf2v_build_csr", "rdf2v_build_walk_edges",
+    "rdf2v_walk_edges_recommended",
     "rdf2v_nonsink_starts_workspace_size",
     "rdf2v_nonsink_starts", "rdf2v_random_walks", "rdf2v_random_walks_tokens",
     "rdf2v_unique_walks_workspace_size", "rdf2v_unique_walks", "rdf2v_bfs_walks_workspace_size",
@@ -80,6 +81,8 @@ def _native():
     lib.rdf2v_build_csr.restype = ctypes.c_int
     lib.rdf2v_build_walk_edges.argtypes = [csr_p, vp, vp, vp]
     lib.rdf2v_build_walk_edges.restype = ctypes.c_int
+    lib.rdf2v_walk_edges_recommended.argtypes = [i32, i64]
+    lib.rdf2v_walk_edges_recommended.restype = i32
     lib.rdf2v_nonsink_starts_workspace_size.argtypes = [i32]
     lib.rdf2v_nonsink_starts_workspace_size.restype = sz
     lib.rdf2v_nonsink_starts.argtypes = [csr_p, vp, vp, vp, sz, vp]
@@ -211,6 +214,12 @@ def rdf2v_build_walk_edges(csr: Csr, *, out: torch.Tensor | None = None,
     st = _native().rdf2v_build_walk_edges(ctypes.byref(c), _ptr(out), _ptr(status), _stream(dev, stream))
     _check(st, "rdf2v_build_walk_edges")
     return Csr(csr.row_ptr, csr.edges, csr.num_entities, csr.num_predicates, out)
+
+
+def rdf2v_walk_edges_recommended(num_entities: int, num_edges: int) -> bool:
+    """Whether rdf2v_build_walk_edges' records are expected to speed up the walks on a CSR of
+    this size (pure host call; the walks are the same either way)."""
+    return bool(_native().rdf2v_walk_edges_recommended(num_entities, num_edges))
 
 
 def rdf2v_nonsink_starts_workspace_size(num_entities: int) -> int:

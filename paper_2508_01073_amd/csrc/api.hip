@@ -62,6 +62,12 @@ RDF2V_API rdf2v_status rdf2v_build_walk_edges(const rdf2v_csr *csr, int32_t *wal
                                   walk_edges_out, status_dev, static_cast<hipStream_t>(stream));
 }
 
+RDF2V_API int32_t rdf2v_walk_edges_recommended(int32_t num_entities, int64_t num_edges) {
+  constexpr int64_t kRowPtrL2Bytes = int64_t(3) << 19;  // 1.5 MiB of row_ptr
+  if (num_entities < 0 || num_edges <= 0) return 0;
+  return (int64_t(num_entities) + 1) * 4 > kRowPtrL2Bytes ? 1 : 0;
+}
+
 RDF2V_API size_t rdf2v_nonsink_starts_workspace_size(int32_t num_entities) {
   return rdf2v::nonsink_workspace_bytes(num_entities);
 }

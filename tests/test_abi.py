@@ -35,7 +35,7 @@ def test_header_declares_the_calls():
               "rdf2v_skipgram_pairs", "rdf2v_skipgram_pairs_workspace_size", "rdf2v_random_walks_tokens",
               "rdf2v_unique_walks", "rdf2v_unique_walks_workspace_size", "rdf2v_bfs_walks",
               "rdf2v_bfs_walks_workspace_size", "rdf2v_build_vocabulary",
-              "rdf2v_build_vocabulary_workspace_size"]:
+              "rdf2v_build_vocabulary_workspace_size", "rdf2v_walk_edges_recommended"]:
         assert n in names
 
 
@@ -55,6 +55,21 @@ def test_header_compiles_as_c():
     res = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-x", "c", HEADER],
                          stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     assert res.returncode == 0, res.stdout
+
+
+def test_walk_edges_recommendation(lib):
+    so, pkg = lib
+    # records pay once row_ptr (4 * (V + 1) bytes) outgrows 1.5 MiB
+    limit = (3 << 19) // 4 - 1  # largest V whose row_ptr fits
+    assert not pkg.rdf2v_walk_edges_recommended(limit, 10**6)
+    assert pkg.rdf2v_walk_edges_recommended(limit + 1, 10**6)
+    assert pkg.rdf2v_walk_edges_recommended(1_000_000, 20_000_000)
+    assert pkg.rdf2v_walk_edges_recommended(50_000_000, 500_000_000)
+    assert not pkg.rdf2v_walk_edges_recommended(100_000, 1_000_000)
+    assert not pkg.rdf2v_walk_edges_recommended(10_000, 10_000_000)
+    assert not pkg.rdf2v_walk_edges_recommended(1_000_000, 0)
+    assert not pkg.rdf2v_walk_edges_recommended(-1, 5)
+    assert so.rdf2v_walk_edges_recommended(2**31 - 1, 2**31 - 1) == 1
 
 
 def test_status_strings(lib):
