@@ -1,0 +1,60 @@
+"""Host logic of bench.py on the CPU: the useful-byte count behind the roofline figure, the
+guard on the committed counter profile, and the one-GPU restriction. No GPU is touched."""
+
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+import torch
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+def test_useful_bytes_hand_counted():
+    # depth 2 (rows of 5 tokens): a full walk (2 hops), one stopped at a sink after 1 hop,
+    # one whose start is a sink (0 hops); 2 start entities read
+    lens = torch.tensor([5, 3, 1], dtype=torch.int32)
+    ub, hops, tokens = bench.useful_bytes(lens, depth=2, num_start=2)
+    assert (hops, tokens) == (3, 9)
+    gathered = 16 * 3 + 8 * 2 + 4 * 2  # per hop, per early stop, per start
+    written = 3 * (4 * 5 + 4)          # padded rows and lengths
+    assert ub == gathered + written
+
+
+def test_useful_bytes_entity_rows():
+    # entity or property rows hold depth + 1 tokens and one token per hop
+    lens = torch.tensor([4, 2], dtype=torch.int32)
+    ub, hops, tokens = bench.useful_bytes(lens, depth=3, num_start=1, kind=1)
+    assert (hops, tokens) == (4, 6)
+    assert ub == 16 * 4 + 8 * 1 + 4 * 1 + 2 * (4 * 4 + 4)
+
+
+def test_traffic_only_for_matching_profile():
+    with open(bench.PMC_FILE) as fh:
+        pmc = json.load(fh)
+    got = bench.traffic_from_profile(pmc["workload"], pmc["num_walks"])
+    if pmc["kernel_source_hash"] == bench.kernel_source_hash():
+        assert got == pmc["hbm_bytes_per_launch"]
+        # the copy calibration: each counter scaled by what it reads for a copy of known size
+        assert pmc["fetch_scale"] == pytest.approx(pmc["copy_bytes"] / 1024 / pmc["copy_fetch_size_kib"])
+        assert pmc["write_scale"] == pytest.approx(pmc["copy_bytes"] / 1024 / pmc["copy_write_size_kib"])
+        expect = (pmc["fetch_size_kib_per_launch"] * pmc["fetch_scale"] +
+                  pmc["write_size_kib_per_launch"] * pmc["write_scale"]) * 1024
+        assert pmc["hbm_bytes_per_launch"] == pytest.approx(expect)
+    else:
+        assert got is None  # counters taken from other kernel sources are not reported
+    assert bench.traffic_from_profile("uniform_1m", pmc["num_walks"]) is None
+    assert bench.traffic_from_profile(pmc["workload"], pmc["num_walks"] + 1) is None
+
+
+def test_more_than_one_gpu_is_refused():
+    res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                         stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=120)
+    assert res.returncode == 2
+    assert "one GPU" in res.stderr
+    assert res.stdout == ""
