@@ -138,6 +138,15 @@ def _dev_i32(t: torch.Tensor, name: str) -> torch.Tensor:
     return t
 
 
+def _ws_bytes(t: torch.Tensor | None) -> int:
+    """Size in bytes of a caller workspace (any dtype; contiguous device memory)."""
+    if t is None:
+        return 0
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or not t.is_contiguous():
+        raise TypeError("workspace must be a contiguous CUDA (HIP) tensor")
+    return t.numel() * t.element_size()
+
+
 def _ptr(t: torch.Tensor | None):
     return None if t is None or t.numel() == 0 else ctypes.c_void_p(t.data_ptr())
 
@@ -193,7 +202,7 @@ def rdf2v_build_csr(subj: torch.Tensor, pred: torch.Tensor, obj: torch.Tensor, n
     need = rdf2v_build_csr_workspace_size(t, num_entities)
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    ws_bytes = _ws_bytes(workspace)
     st = _native().rdf2v_build_csr(_ptr(subj), _ptr(pred), _ptr(obj), t, num_entities, num_predicates,
                               _ptr(row_ptr), _ptr(edges), _ptr(workspace), ws_bytes, _ptr(status),
                               _stream(dev, stream))
@@ -241,7 +250,7 @@ def rdf2v_nonsink_starts(csr: Csr, *, workspace: torch.Tensor | None = None, str
                                 dtype=torch.uint8, device=dev)
     c = csr._c()
     st = _native().rdf2v_nonsink_starts(ctypes.byref(c), _ptr(starts), _ptr(count), _ptr(workspace),
-                                   workspace.numel(), _stream(dev, stream))
+                                   _ws_bytes(workspace), _stream(dev, stream))
     _check(st, "rdf2v_nonsink_starts")
     if not sync:
         return starts, count
@@ -316,7 +325,7 @@ def rdf2v_unique_walks(tokens: torch.Tensor, lens: torch.Tensor, group_size: int
     if workspace is None:
         workspace = torch.empty(max(rdf2v_unique_walks_workspace_size(n), 1), dtype=torch.uint8, device=dev)
     st = _native().rdf2v_unique_walks(_ptr(tokens), _ptr(lens), n, group_size, width, _ptr(tokens_out),
-                                      _ptr(lens_out), _ptr(count), _ptr(workspace), workspace.numel(),
+                                      _ptr(lens_out), _ptr(count), _ptr(workspace), _ws_bytes(workspace),
                                       _ptr(status), _stream(dev, stream))
     _check(st, "rdf2v_unique_walks")
     if not sync:
@@ -350,7 +359,7 @@ def rdf2v_bfs_walks(csr: Csr, roots: torch.Tensor, depth: int, max_walks: int, *
                                 dtype=torch.uint8, device=dev)
     c = csr._c()
     st = _native().rdf2v_bfs_walks(ctypes.byref(c), _ptr(roots), R, depth, max_walks, _ptr(tokens), _ptr(lens),
-                                   _ptr(counts), _ptr(workspace), workspace.numel(), _ptr(status),
+                                   _ptr(counts), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
                                    _stream(dev, stream))
     _check(st, "rdf2v_bfs_walks")
     return tokens, lens, counts
@@ -380,7 +389,7 @@ def rdf2v_skipgram_pairs(tokens: torch.Tensor, lens: torch.Tensor, window: int, 
 
     def call(out, cap):
         st = _native().rdf2v_skipgram_pairs(_ptr(tokens), _ptr(lens), w, width, window, _ptr(out), cap,
-                                          _ptr(count), _ptr(workspace), workspace.numel(), _ptr(status),
+                                          _ptr(count), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
                                           _stream(dev, stream))
         _check(st, "rdf2v_skipgram_pairs")
 
@@ -433,7 +442,7 @@ def rdf2v_build_vocabulary(subj, pred, obj, max_entities: int, max_predicates: i
         need = rdf2v_build_vocabulary_workspace_size(n, max_entities, max_predicates)
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     st = _native().rdf2v_build_vocabulary(*args, n, max_entities, max_predicates, *[_ptr(i) for i in ids],
-                                          _ptr(counts), _ptr(workspace), workspace.numel(), _ptr(status),
+                                          _ptr(counts), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
                                           _stream(dev, stream))
     _check(st, "rdf2v_build_vocabulary")
     return ids[0], ids[1], ids[2], counts
