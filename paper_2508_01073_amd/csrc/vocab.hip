@@ -283,7 +283,9 @@ __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot
   const int64_t q = q0 + tid;
   const bool active = q < n;
   const int col = seq_col<kPaired>(q);
-  const StrCol &c = seq.col[col];
+  // Both columns' descriptors are kernel arguments; pick by value so they stay
+  // scalar loads instead of a per-lane indexed load before the offsets.
+  const StrCol c = (kPaired && col == 1) ? seq.col[kCols - 1] : seq.col[0];
   if constexpr (kGroupEqual) {
     for (int i = tid; i < kLocal; i += kBlock) {
       loc_owner[i] = 0;
@@ -306,9 +308,14 @@ __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot
     len = b - a;
   }
   __syncthreads();
-  // Stage that span in LDS when it fits.
+  // Stage that span in LDS when it fits. Every load of every column is issued
+  // before the first LDS store, so the stage costs one memory round trip
+  // rather than one per kBlock words; words that reach past the column's last
+  // byte are rebuilt bytewise afterwards.
+  constexpr int kStageLoads = (kPerCol - kPad + kBlock - 1) / kBlock;
   int64_t base[kCols];
   int32_t count[kCols];
+  uint32_t staged[kCols][kStageLoads];
 #pragma unroll
   for (int cc = 0; cc < kCols; ++cc) {
     const int64_t lo = span[cc][0], hi = span[cc][1];
@@ -316,8 +323,24 @@ __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot
     base[cc] = ok ? (lo >> 2) : 0;
     const int64_t words = ok ? ((hi + 3) >> 2) - base[cc] : -1;
     count[cc] = (words >= 0 && words <= kPerCol - kPad) ? int32_t(words) : -1;
+    const uint32_t *src = reinterpret_cast<const uint32_t *>(seq.col[cc].chars);
+    const int64_t whole = seq.col[cc].bytes >> 2;  // words that lie entirely inside the column
+#pragma unroll
+    for (int j = 0; j < kStageLoads; ++j) {
+      const int32_t i = tid + j * kBlock;
+      const int64_t g = base[cc] + i;
+      staged[cc][j] = (i < count[cc] && g < whole) ? src[g] : 0u;
+    }
+  }
+#pragma unroll
+  for (int cc = 0; cc < kCols; ++cc) {
     uint32_t *dst = stage + cc * kPerCol;
-    for (int32_t i = tid; i < count[cc]; i += kBlock) dst[i] = load_word(seq.col[cc], base[cc] + i);
+    const int64_t whole = seq.col[cc].bytes >> 2;
+#pragma unroll
+    for (int j = 0; j < kStageLoads; ++j) {
+      const int32_t i = tid + j * kBlock;
+      if (i < count[cc]) dst[i] = base[cc] + i < whole ? staged[cc][j] : load_word(seq.col[cc], base[cc] + i);
+    }
     if (count[cc] >= 0 && tid < kPad) dst[count[cc] + tid] = 0;
   }
   __syncthreads();
@@ -336,7 +359,7 @@ __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot
   for (int i = 0; i < nw; ++i) h = hash_step(h, word7_lds(lds, at, len, i));
   h = fmix64(h);
 
-  int32_t *out = seq.out[col] + seq_row<kPaired>(q);
+  int32_t *out = ((kPaired && col == 1) ? seq.out[kCols - 1] : seq.out[0]) + seq_row<kPaired>(q);
   if constexpr (!kGroupEqual) {
     if (fast) {
       const int32_t r = find_or_claim(table, mask, h, q, lds, at, len);
@@ -406,9 +429,10 @@ __global__ __launch_bounds__(kThreads) void insert_general_kernel(Seq seq, int64
   const int64_t q = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   if (q >= n) return;
   const int col = seq_col<kPaired>(q);
-  int32_t *out = seq.out[col] + seq_row<kPaired>(q);
+  int32_t *out = ((kPaired && col == 1) ? seq.out[1] : seq.out[0]) + seq_row<kPaired>(q);
   if (*out != kDeferred) return;
-  const StrCol *c = &seq.col[col];
+  const StrCol cv = (kPaired && col == 1) ? seq.col[1] : seq.col[0];
+  const StrCol *c = &cv;
   int bad = 0;
   int64_t start, len;
   string_range(*c, seq_row<kPaired>(q), start, len, bad);
