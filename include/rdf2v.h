@@ -198,7 +198,9 @@ rdf2v_status rdf2v_random_walks(const rdf2v_csr *csr, const int32_t *start_nodes
                                 int64_t walk_begin, int64_t walk_count, int32_t *tokens_out,
                                 int32_t *len_out, int32_t *status_dev, void *stream);
 
-/* Bytes of device workspace rdf2v_skipgram_pairs needs. Pure host function. */
+/* Bytes of device workspace rdf2v_skipgram_pairs needs. Pure host function;
+ * 0 when num_walks is negative or above 2^46 (rdf2v_skipgram_pairs returns
+ * RDF2V_ERR_TOO_LARGE for more rows). */
 size_t rdf2v_skipgram_pairs_workspace_size(int64_t num_walks);
 
 /*
@@ -253,7 +255,9 @@ rdf2v_status rdf2v_random_walks_tokens(const rdf2v_csr *csr, const int32_t *star
                                        int32_t token_kind, int32_t *tokens_out, int32_t *len_out,
                                        int32_t *status_dev, void *stream);
 
-/* Bytes of device workspace rdf2v_unique_walks needs. Pure host function. */
+/* Bytes of device workspace rdf2v_unique_walks needs. Pure host function;
+ * 0 when num_walks is negative or above 255 * 2^31 (rdf2v_unique_walks
+ * returns RDF2V_ERR_TOO_LARGE for more rows). */
 size_t rdf2v_unique_walks_workspace_size(int64_t num_walks);
 
 /*
@@ -276,7 +280,9 @@ rdf2v_status rdf2v_unique_walks(const int32_t *tokens, const int32_t *len, int64
                                 int32_t *len_out, int64_t *count_out, void *workspace,
                                 size_t workspace_bytes, int32_t *status_dev, void *stream);
 
-/* Bytes of device workspace rdf2v_bfs_walks needs. Pure host function. */
+/* Bytes of device workspace rdf2v_bfs_walks needs. Pure host function;
+ * 0 when a size is negative or num_roots >= 2^31 (rdf2v_bfs_walks returns
+ * RDF2V_ERR_TOO_LARGE for that many roots). */
 size_t rdf2v_bfs_walks_workspace_size(int32_t num_entities, int64_t num_roots);
 
 /*
@@ -355,8 +361,9 @@ rdf2v_status rdf2v_build_vocabulary(const uint8_t *subj_chars, const int64_t *su
                                     int32_t *subj_ids, int32_t *pred_ids, int32_t *obj_ids, int64_t *counts_out,
                                     void *workspace, size_t workspace_bytes, int32_t *status_dev, void *stream);
 
-/* Static, human-readable name of a status code. */
-const char *rdf2v_status_string(rdf2v_status status);
+/* Static, human-readable name of a status code (any int: values that are not
+ * an rdf2v_status give "RDF2V_UNKNOWN_STATUS"). */
+const char *rdf2v_status_string(int status);
 
 #ifdef __cplusplus
 }

@@ -9,6 +9,11 @@
 namespace {
 
 constexpr int64_t kInt32Limit = int64_t(1) << 31;
+// Most walk rows one skip-gram call takes: far beyond any device memory, and
+// small enough that workspace sizes and pair offsets (fewer than 2^15 pairs
+// per row) stay exact in 64 bits.
+constexpr int64_t kMaxRows = int64_t(1) << 46;
+constexpr int64_t kMaxUniqueRows = (int64_t(1) << 31) * 255;  // block counts fit the compaction's index type
 
 bool id_space_too_large(int32_t num_entities, int32_t num_predicates) {
   return int64_t(num_entities) + int64_t(num_predicates) >= kInt32Limit;
@@ -146,7 +151,7 @@ RDF2V_API rdf2v_status rdf2v_random_walks_tokens(const rdf2v_csr *csr, const int
 }
 
 RDF2V_API size_t rdf2v_skipgram_pairs_workspace_size(int64_t num_walks) {
-  if (num_walks < 0) return 0;
+  if (num_walks < 0 || num_walks > kMaxRows) return 0;
   return rdf2v::skipgram_workspace_bytes(num_walks);
 }
 
@@ -161,7 +166,7 @@ RDF2V_API rdf2v_status rdf2v_skipgram_pairs(const int32_t *tokens, const int32_t
   if (num_walks > 0 && (tokens == nullptr || len == nullptr)) return RDF2V_ERR_INVALID_ARGUMENT;
   if (pair_capacity > 0 && pairs_out == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
   if ((reinterpret_cast<uintptr_t>(pairs_out) & 7) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
-  if (num_walks > INT64_MAX / (2 * int64_t(row_width))) return RDF2V_ERR_TOO_LARGE;
+  if (num_walks > kMaxRows) return RDF2V_ERR_TOO_LARGE;
   const size_t need = rdf2v::skipgram_workspace_bytes(num_walks);
   if (workspace == nullptr || workspace_bytes < need) return RDF2V_ERR_WORKSPACE;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return RDF2V_ERR_WORKSPACE;
@@ -171,7 +176,7 @@ RDF2V_API rdf2v_status rdf2v_skipgram_pairs(const int32_t *tokens, const int32_t
 }
 
 RDF2V_API size_t rdf2v_unique_walks_workspace_size(int64_t num_walks) {
-  if (num_walks < 0) return 0;
+  if (num_walks < 0 || num_walks > kMaxUniqueRows) return 0;
   return rdf2v::unique_walks_workspace_bytes(num_walks);
 }
 
@@ -183,7 +188,7 @@ RDF2V_API rdf2v_status rdf2v_unique_walks(const int32_t *tokens, const int32_t *
   if (count_out == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
   if (num_walks > 0 && (tokens == nullptr || len == nullptr || tokens_out == nullptr || len_out == nullptr))
     return RDF2V_ERR_INVALID_ARGUMENT;
-  if (num_walks > (int64_t(1) << 31) * 255 || num_walks > INT64_MAX / row_width) return RDF2V_ERR_TOO_LARGE;
+  if (num_walks > kMaxUniqueRows || num_walks > INT64_MAX / row_width) return RDF2V_ERR_TOO_LARGE;
   const size_t need = rdf2v::unique_walks_workspace_bytes(num_walks);
   if (workspace == nullptr || workspace_bytes < need) return RDF2V_ERR_WORKSPACE;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return RDF2V_ERR_WORKSPACE;
@@ -192,7 +197,8 @@ RDF2V_API rdf2v_status rdf2v_unique_walks(const int32_t *tokens, const int32_t *
 }
 
 RDF2V_API size_t rdf2v_bfs_walks_workspace_size(int32_t num_entities, int64_t num_roots) {
-  if (num_entities < 0 || num_roots < 0) return 0;
+  // rdf2v_bfs_walks takes fewer than 2^31 roots (its per-level stamps are int32)
+  if (num_entities < 0 || num_roots < 0 || num_roots >= kInt32Limit) return 0;
   return rdf2v::bfs_walks_workspace_bytes(num_entities, num_roots);
 }
 
@@ -206,8 +212,9 @@ RDF2V_API rdf2v_status rdf2v_bfs_walks(const rdf2v_csr *csr, const int32_t *root
   if (num_roots < 0 || depth < 0 || depth > RDF2V_MAX_DEPTH || max_walks < 1) return RDF2V_ERR_INVALID_ARGUMENT;
   if (csr->num_edges >= kInt32Limit || id_space_too_large(csr->num_entities, csr->num_predicates))
     return RDF2V_ERR_TOO_LARGE;
-  // the per-level stamps of one workgroup must not run out
-  if (num_roots > 0 && (num_roots + 1) * int64_t(depth + 1) >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
+  // the per-level stamps of one workgroup (int32) must not run out
+  if (num_roots >= kInt32Limit || (num_roots > 0 && (num_roots + 1) * int64_t(depth + 1) >= kInt32Limit))
+    return RDF2V_ERR_TOO_LARGE;
   if (num_roots > INT64_MAX / max_walks / (2 * int64_t(depth) + 1)) return RDF2V_ERR_TOO_LARGE;
   if (num_roots == 0) return RDF2V_OK;
   if (roots == nullptr || tokens_out == nullptr || len_out == nullptr || counts_out == nullptr)
@@ -275,7 +282,7 @@ RDF2V_API rdf2v_status rdf2v_build_vocabulary(const uint8_t *subj_chars, const i
                                         static_cast<hipStream_t>(stream));
 }
 
-RDF2V_API const char *rdf2v_status_string(rdf2v_status status) {
+RDF2V_API const char *rdf2v_status_string(int status) {
   switch (status) {
     case RDF2V_OK: return "RDF2V_OK";
     case RDF2V_ERR_INVALID_ARGUMENT: return "RDF2V_ERR_INVALID_ARGUMENT";
