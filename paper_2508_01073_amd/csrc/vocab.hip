@@ -71,6 +71,19 @@ struct Seq {
   int32_t *out[2];
 };
 
+// A value that is the same in every lane, held as such (readfirstlane), so
+// that a per-lane choice between two of them stays a register select.
+__device__ __forceinline__ uint64_t uniform_u64(uint64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(v));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(v >> 32));
+  return (uint64_t(hi) << 32) | lo;
+}
+__device__ __forceinline__ StrCol uniform_col(const StrCol &c) {
+  return {reinterpret_cast<const uint8_t *>(uniform_u64(reinterpret_cast<uintptr_t>(c.chars))),
+          reinterpret_cast<const int64_t *>(uniform_u64(reinterpret_cast<uintptr_t>(c.off))),
+          int64_t(uniform_u64(uint64_t(c.bytes)))};
+}
+
 template <bool kPaired>
 __device__ __forceinline__ int seq_col(int64_t q) {
   return kPaired ? int(q & 1) : 0;
@@ -283,9 +296,10 @@ __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot
   const int64_t q = q0 + tid;
   const bool active = q < n;
   const int col = seq_col<kPaired>(q);
-  // Both columns' descriptors are kernel arguments; pick by value so they stay
-  // scalar loads instead of a per-lane indexed load before the offsets.
-  const StrCol c = (kPaired && col == 1) ? seq.col[kCols - 1] : seq.col[0];
+  // Both columns' descriptors are kernel arguments: read them as wave-uniform
+  // values and pick per lane, rather than loading through a per-lane address
+  // (one more memory round trip before the offsets).
+  const StrCol c = (kPaired && col == 1) ? uniform_col(seq.col[kCols - 1]) : uniform_col(seq.col[0]);
   if constexpr (kGroupEqual) {
     for (int i = tid; i < kLocal; i += kBlock) {
       loc_owner[i] = 0;
