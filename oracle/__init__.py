@@ -81,6 +81,9 @@ def _load():
     lib.rdf2v_ref_skipgram_pairs.argtypes = [i32p, i32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                              i32p, ctypes.c_int64]
     lib.rdf2v_ref_skipgram_pairs.restype = ctypes.c_int64
+    lib.rdf2v_ref_cbow_examples.argtypes = [i32p, i32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                            i32p, i32p, ctypes.c_int64]
+    lib.rdf2v_ref_cbow_examples.restype = ctypes.c_int64
     _lib = lib
     return lib
 
@@ -187,6 +190,22 @@ def skipgram_pairs(tokens, lens, window: int) -> np.ndarray:
     pairs = np.empty((n, 2), dtype=np.int32)
     lib.rdf2v_ref_skipgram_pairs(_ptr(tok), _ptr(ln), w, width, window, _ptr(pairs), n)
     return pairs
+
+
+def cbow_examples(tokens, lens, window: int):
+    """CBOW examples of walk rows tokens[W, width] with lens[W] valid tokens: (centers[N],
+    contexts[N, 2*window]) for every valid position, contexts ascending, padded with -1."""
+    lib = _load()
+    tok = _i32(tokens)
+    ln = _i32(lens)
+    w, width = (tok.shape[0], tok.shape[1]) if tok.ndim == 2 else (ln.shape[0], 1)
+    n = lib.rdf2v_ref_cbow_examples(_ptr(tok), _ptr(ln), w, width, window, None, None, 0)
+    if n < 0:
+        raise OracleError(int(-n), "rdf2v_ref_cbow_examples")
+    centers = np.empty(n, dtype=np.int32)
+    contexts = np.empty((n, 2 * window), dtype=np.int32)
+    lib.rdf2v_ref_cbow_examples(_ptr(tok), _ptr(ln), w, width, window, _ptr(centers), _ptr(contexts), n)
+    return centers, contexts
 
 
 ENTITY_WALKS = 1

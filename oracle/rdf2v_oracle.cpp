@@ -408,4 +408,35 @@ int64_t rdf2v_ref_skipgram_pairs(const int32_t *tokens, const int32_t *len, int6
   return n;
 }
 
+// CBOW training examples (Sec. 3.2: the library trains Continuous Bag of
+// Words next to Skip-Gram; CBOW predicts a center token from the tokens around
+// it). For walk r with L = len[r] valid tokens t_0 .. t_{L-1}, every position i
+// gives one example: centers[e] = t_i and contexts[e][0 .. 2*window) = the t_j
+// with 1 <= |i - j| <= window and 0 <= j < L in ascending j, then -1 up to
+// 2*window entries. Examples in the order walk, then i. Returns the number of
+// examples (the sum of the lengths); writes at most `capacity` of them. A
+// negative return is an argument error.
+int64_t rdf2v_ref_cbow_examples(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                int32_t row_width, int32_t window, int32_t *centers, int32_t *contexts,
+                                int64_t capacity) {
+  if (num_walks < 0 || row_width < 1 || window < 1 || capacity < 0) return -REF_ERR_INVALID_ARGUMENT;
+  const int64_t ctx_width = 2 * int64_t(window);
+  int64_t e = 0;
+  for (int64_t r = 0; r < num_walks; ++r) {
+    const int32_t *row = tokens + r * row_width;
+    const int64_t L = len[r];
+    if (L < 0 || L > row_width) return -REF_ERR_INVALID_ARGUMENT;
+    for (int64_t i = 0; i < L; ++i, ++e) {
+      if (e >= capacity) continue;
+      centers[e] = row[i];
+      int32_t *ctx = contexts + e * ctx_width;
+      int64_t m = 0;
+      for (int64_t j = i - window; j <= i + window; ++j)
+        if (j != i && j >= 0 && j < L) ctx[m++] = row[j];
+      for (; m < ctx_width; ++m) ctx[m] = -1;
+    }
+  }
+  return e;
+}
+
 }  // extern "C"
