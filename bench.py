@@ -152,6 +152,47 @@ def cpu_baseline_threads(oracle, rp, ed, V, P, starts, w, rate_1t: float, second
             "sample": f"walks [0, {n * per_thread:,}) in {n} disjoint ranges, {elapsed:.2f} s wall (walks only)"}
 
 
+def time_cbow(rd, torch, tokens, lens, n_walks, batch_cap, width, window, batch, stream, ev):
+    """Time rdf2v_cbow_examples over the walk rows left in the output buffer, in batches of
+    `batch` walks into one reused pair of output buffers.
+
+    Algorithmic bytes: each walk row and its length are read once (4 * width + 4 B) and every
+    example is written once (a 4-byte center and 2 * window 4-byte contexts)."""
+    dev = tokens.device
+    rows = min(n_walks, batch_cap)
+    batch = min(batch, rows)
+    cap = batch * width  # at most one example per token
+    centers = torch.empty(cap, dtype=torch.int32, device=dev)
+    contexts = torch.empty((cap, 2 * window), dtype=torch.int32, device=dev)
+    ws = torch.empty(rd.rdf2v_cbow_examples_workspace_size(batch), dtype=torch.uint8, device=dev)
+    count = torch.empty(1, dtype=torch.int64, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    total = 0
+    for b0 in range(0, rows, batch):  # warm-up pass that also counts
+        c = min(batch, rows - b0)
+        rd.rdf2v_cbow_examples(tokens[b0:b0 + c], lens[b0:b0 + c], window, centers=centers, contexts=contexts,
+                               count=count, workspace=ws, status=status, stream=stream)
+        torch.cuda.synchronize()
+        total += int(count.item())
+    rd.check_device_status(status, "cbow examples")
+    e0, e1 = ev(), ev()
+    e0.record(stream)
+    for b0 in range(0, rows, batch):
+        c = min(batch, rows - b0)
+        rd.rdf2v_cbow_examples(tokens[b0:b0 + c], lens[b0:b0 + c], window, centers=centers, contexts=contexts,
+                               count=count, workspace=ws, status=status, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    useful = rows * (4 * width + 4) + total * (4 + 8 * window)
+    return {
+        "window": window, "walks": rows, "examples": total, "batch_walks": batch,
+        "ms": ms, "examples_per_s": total / (ms * 1e-3),
+        "useful_bytes": useful, "achieved_GBps": useful / (ms * 1e-3) / 1e9,
+        "frac_of_hbm_peak": useful / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+    }
+
+
 def time_pairs(rd, torch, tokens, lens, n_walks, batch_cap, width, window, pair_batch, stream, ev):
     """Time rdf2v_skipgram_pairs over the walk rows left in the output buffer (the whole corpus
     when it was produced in one launch), in batches of `pair_batch` walks.
@@ -314,6 +355,8 @@ def main() -> int:
                     help="also time skip-gram pair generation over the corpus with this window "
                          "(0: off)")
     ap.add_argument("--pairs-batch-walks", type=int, default=8_000_000)
+    ap.add_argument("--cbow-window", type=int, default=0,
+                    help="after the timed steps, also time rdf2v_cbow_examples over the corpus with this window")
     ap.add_argument("--vocab", action="store_true",
                     help="also time the vocabulary (string triples -> ids) on IRI-like labels of "
                          "the workload's triples")
@@ -488,6 +531,9 @@ def main() -> int:
     if args.pairs_window > 0:
         out["skipgram_pairs"] = time_pairs(rd, torch, tokens, lens, n_walks, batch_cap, width,
                                            args.pairs_window, args.pairs_batch_walks, stream, ev)
+    if args.cbow_window > 0:
+        out["cbow_examples"] = time_cbow(rd, torch, tokens, lens, n_walks, batch_cap, width, args.cbow_window,
+                                         args.pairs_batch_walks, stream, ev)
     if args.vocab:
         out["vocabulary"] = time_vocab(rd, torch, synth, w, s, p, o, stream, ev)
     if not args.no_cpu_baseline:

@@ -233,6 +233,44 @@ rdf2v_status rdf2v_skipgram_pairs(const int32_t *tokens, const int32_t *len, int
                                   int64_t pair_capacity, int64_t *pair_count_out, void *workspace,
                                   size_t workspace_bytes, int32_t *status_dev, void *stream);
 
+/* Bytes of device workspace rdf2v_cbow_examples needs. Pure host function;
+ * 0 when num_walks is negative or above 2^46 (rdf2v_cbow_examples returns
+ * RDF2V_ERR_TOO_LARGE for more rows). */
+size_t rdf2v_cbow_examples_workspace_size(int64_t num_walks);
+
+/*
+ * CBOW training examples from walk rows (gpuRDF2vec Sec. 3.2: the library
+ * trains Continuous Bag of Words next to Skip-Gram; CBOW predicts a center
+ * token from the tokens around it; Sec. 3.1: the -1 padding is dropped).
+ *
+ * For walk r with L = len[r] valid tokens t_0 .. t_{L-1}, every position i
+ * gives one example: the center t_i and its contexts, the t_j with
+ * 1 <= |i - j| <= window and 0 <= j < L in ascending j, followed by -1 up to
+ * 2 * window entries. Examples are ordered by walk, then i; a walk of L tokens
+ * gives L examples (a one-token walk gives one with no context). Read in order,
+ * the (center, context) of the non-padding contexts are exactly the pairs of
+ * rdf2v_skipgram_pairs with the same window.
+ *
+ *   tokens, len, row_width  as for rdf2v_skipgram_pairs.
+ *   window          1 .. 2 * RDF2V_MAX_DEPTH.
+ *   centers_out     [capacity] int32 (device); may be NULL when capacity == 0.
+ *   contexts_out    [capacity][2 * window] int32 (device), row-major; may be
+ *                   NULL when capacity == 0.
+ *   count_out       one int64 in device memory: the number of examples (the sum
+ *                   of the lengths), also when it exceeds capacity (then only
+ *                   the first capacity examples are written and
+ *                   RDF2V_STATUS_CAPACITY is raised).
+ *   workspace       device scratch, rdf2v_cbow_examples_workspace_size() bytes,
+ *                   256-byte aligned.
+ *   status_dev      device int32 or NULL (RDF2V_STATUS_BAD_LENGTH for a length
+ *                   outside [0, row_width], treated as clamped;
+ *                   RDF2V_STATUS_CAPACITY).
+ */
+rdf2v_status rdf2v_cbow_examples(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                 int32_t row_width, int32_t window, int32_t *centers_out, int32_t *contexts_out,
+                                 int64_t capacity, int64_t *count_out, void *workspace, size_t workspace_bytes,
+                                 int32_t *status_dev, void *stream);
+
 /* Which tokens a walk row holds (Tab. 1 lists entity walks and property walks
  * beside triple-based random walks). All three follow the same walk, drawn
  * from the same random stream, so an entity or property walk is exactly the

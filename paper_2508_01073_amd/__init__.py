@@ -30,7 +30,8 @@ __all__ = [
     "rdf2v_nonsink_starts", "rdf2v_random_walks", "rdf2v_random_walks_tokens",
     "rdf2v_unique_walks_workspace_size", "rdf2v_unique_walks", "rdf2v_bfs_walks_workspace_size",
     "rdf2v_bfs_walks", "rdf2v_skipgram_pairs_workspace_size",
-    "rdf2v_skipgram_pairs", "rdf2v_build_vocabulary_workspace_size", "rdf2v_build_vocabulary",
+    "rdf2v_skipgram_pairs", "rdf2v_cbow_examples_workspace_size", "rdf2v_cbow_examples",
+    "rdf2v_build_vocabulary_workspace_size", "rdf2v_build_vocabulary",
     "rdf2v_status_string", "check_device_status",
     "library_path",
 ]
@@ -103,6 +104,10 @@ def _native():
     lib.rdf2v_skipgram_pairs_workspace_size.restype = sz
     lib.rdf2v_skipgram_pairs.argtypes = [vp, vp, i64, i32, i32, vp, i64, vp, vp, sz, vp, vp]
     lib.rdf2v_skipgram_pairs.restype = ctypes.c_int
+    lib.rdf2v_cbow_examples_workspace_size.argtypes = [i64]
+    lib.rdf2v_cbow_examples_workspace_size.restype = sz
+    lib.rdf2v_cbow_examples.argtypes = [vp, vp, i64, i32, i32, vp, vp, i64, vp, vp, sz, vp, vp]
+    lib.rdf2v_cbow_examples.restype = ctypes.c_int
     lib.rdf2v_build_vocabulary_workspace_size.argtypes = [i64, i64, i64]
     lib.rdf2v_build_vocabulary_workspace_size.restype = sz
     lib.rdf2v_build_vocabulary.argtypes = [vp, vp, i64] * 3 + [i64, i64, i64, vp, vp, vp, vp, vp, sz, vp, vp]
@@ -401,6 +406,53 @@ def rdf2v_skipgram_pairs(tokens: torch.Tensor, lens: torch.Tensor, window: int, 
     out = torch.empty((n, 2), dtype=torch.int32, device=dev)
     call(out, n)
     return out
+
+
+def rdf2v_cbow_examples_workspace_size(num_walks: int) -> int:
+    return int(_native().rdf2v_cbow_examples_workspace_size(num_walks))
+
+
+def rdf2v_cbow_examples(tokens: torch.Tensor, lens: torch.Tensor, window: int, *,
+                        centers: torch.Tensor | None = None, contexts: torch.Tensor | None = None,
+                        count: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                        status: torch.Tensor | None = None, stream=None):
+    """Walk rows tokens [W, width] + lens [W] -> CBOW examples: centers [N] int32 and contexts
+    [N, 2*window] int32 (ascending, padded with -1), one example per valid token.
+
+    With `centers` and `contexts` given (capacity = their rows), writes at most that many
+    examples and returns (centers, contexts, count) with the device int64 total (no host
+    synchronisation). Without them, a first call counts, the host reads the count, and a second
+    call fills tensors of exactly that size, which are returned as (centers, contexts)."""
+    _dev_i32(tokens, "tokens"); _dev_i32(lens, "lens")
+    dev = tokens.device
+    w = int(lens.shape[0])
+    width = int(tokens.shape[1]) if tokens.dim() == 2 else 1
+    if workspace is None:
+        workspace = torch.empty(max(rdf2v_cbow_examples_workspace_size(w), 1), dtype=torch.uint8, device=dev)
+    if count is None:
+        count = torch.empty(1, dtype=torch.int64, device=dev)
+
+    def call(c, x, cap):
+        st = _native().rdf2v_cbow_examples(_ptr(tokens), _ptr(lens), w, width, window, _ptr(c), _ptr(x), cap,
+                                           _ptr(count), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
+                                           _stream(dev, stream))
+        _check(st, "rdf2v_cbow_examples")
+
+    if (centers is None) != (contexts is None):
+        raise ValueError("give both centers and contexts, or neither")
+    if centers is not None:
+        _dev_i32(centers, "centers"); _dev_i32(contexts, "contexts")
+        cap = int(centers.shape[0])
+        if contexts.numel() < cap * 2 * window:
+            raise ValueError("contexts must hold 2 * window entries per center")
+        call(centers, contexts, cap)
+        return centers, contexts, count
+    call(None, None, 0)
+    n = int(count.item())
+    c = torch.empty(n, dtype=torch.int32, device=dev)
+    x = torch.empty((n, 2 * window), dtype=torch.int32, device=dev)
+    call(c, x, n)
+    return c, x
 
 
 def rdf2v_build_vocabulary_workspace_size(num_triples: int, max_entities: int, max_predicates: int) -> int:

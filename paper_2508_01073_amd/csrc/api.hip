@@ -175,6 +175,32 @@ RDF2V_API rdf2v_status rdf2v_skipgram_pairs(const int32_t *tokens, const int32_t
                                       static_cast<hipStream_t>(stream));
 }
 
+RDF2V_API size_t rdf2v_cbow_examples_workspace_size(int64_t num_walks) {
+  if (num_walks < 0 || num_walks > kMaxRows) return 0;
+  return rdf2v::skipgram_workspace_bytes(num_walks);  // the same per-walk offsets and block sums
+}
+
+RDF2V_API rdf2v_status rdf2v_cbow_examples(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                           int32_t row_width, int32_t window, int32_t *centers_out,
+                                           int32_t *contexts_out, int64_t capacity, int64_t *count_out,
+                                           void *workspace, size_t workspace_bytes, int32_t *status_dev,
+                                           void *stream) {
+  if (num_walks < 0 || capacity < 0) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (window < 1 || window > 2 * RDF2V_MAX_DEPTH) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (row_width < 1 || row_width > 2 * RDF2V_MAX_DEPTH + 1) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (count_out == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (num_walks > 0 && (tokens == nullptr || len == nullptr)) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (capacity > 0 && (centers_out == nullptr || contexts_out == nullptr)) return RDF2V_ERR_INVALID_ARGUMENT;
+  if (((reinterpret_cast<uintptr_t>(centers_out) | reinterpret_cast<uintptr_t>(contexts_out)) & 3) != 0)
+    return RDF2V_ERR_INVALID_ARGUMENT;
+  if (num_walks > kMaxRows || capacity > kMaxRows * (2 * RDF2V_MAX_DEPTH + 1)) return RDF2V_ERR_TOO_LARGE;
+  const size_t need = rdf2v::skipgram_workspace_bytes(num_walks);
+  if (workspace == nullptr || workspace_bytes < need) return RDF2V_ERR_WORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return RDF2V_ERR_WORKSPACE;
+  return rdf2v::launch_cbow_examples(tokens, len, num_walks, row_width, window, centers_out, contexts_out,
+                                     capacity, count_out, workspace, status_dev, static_cast<hipStream_t>(stream));
+}
+
 RDF2V_API size_t rdf2v_unique_walks_workspace_size(int64_t num_walks) {
   if (num_walks < 0 || num_walks > kMaxUniqueRows) return 0;
   return rdf2v::unique_walks_workspace_bytes(num_walks);

@@ -58,6 +58,9 @@ rdf2v_status launch_walk_edges(const int32_t *row_ptr, const int32_t *edges, int
                                hipStream_t stream);
 
 size_t skipgram_workspace_bytes(int64_t num_walks);
+rdf2v_status launch_cbow_examples(const int32_t *tokens, const int32_t *len, int64_t num_walks, int32_t width,
+                                  int32_t window, int32_t *centers_out, int32_t *contexts_out, int64_t capacity,
+                                  int64_t *count_out, void *workspace, int32_t *status_dev, hipStream_t stream);
 rdf2v_status launch_skipgram_pairs(const int32_t *tokens, const int32_t *len, int64_t num_walks,
                                    int32_t width, int32_t window, int32_t *pairs_out, int64_t capacity,
                                    int64_t *count_out, void *workspace, int32_t *status_dev,

@@ -1,4 +1,4 @@
-// Skip-gram training pairs from walk rows on gfx950.
+// Skip-gram training pairs and CBOW training examples from walk rows on gfx950.
 //
 // gpuRDF2vec turns the walk corpus into center-context pairs for SkipGram
 // (Sec. 3.2) after dropping the -1 padding (Sec. 3.1). For walk r with
@@ -11,6 +11,13 @@
 // exceeds 2^31 pairs) and the emit kernel needs no atomics: one thread per
 // (walk, center) computes where its pairs start, again in closed form, and
 // places them. Pure integer streaming work, bound by HBM writes.
+//
+// CBOW (Sec. 3.2: the library trains Continuous Bag of Words next to
+// Skip-Gram; it predicts a center token from the tokens around it) takes one
+// example per valid token: the center t_i and its contexts, the t_j with
+// 1 <= |i - j| <= window in ascending j, padded with -1 to 2 * window entries.
+// Examples are ordered by walk, then i; a walk of L tokens gives L of them, so
+// the offsets are a scan of the lengths and the same kernels serve both.
 
 #include <algorithm>
 
@@ -40,6 +47,12 @@ __device__ __forceinline__ int64_t capped_prefix(int64_t n, int64_t window) {
   return window * (window + 1) / 2 + (n - 1 - window) * window;
 }
 
+// Training items of one walk of L valid tokens: pairs, or CBOW examples.
+template <bool kCbow>
+__device__ __forceinline__ int64_t walk_items(int64_t L, int64_t window) {
+  return kCbow ? L : walk_pairs(L, window);
+}
+
 // Valid length of walk r, clamped to the row; out-of-range lengths raise a flag.
 __device__ __forceinline__ int32_t clamped_len(const int32_t *len, int64_t r, int32_t width, int &bad) {
   const int32_t L = len[r];
@@ -50,6 +63,7 @@ __device__ __forceinline__ int32_t clamped_len(const int32_t *len, int64_t r, in
   return L;
 }
 
+template <bool kCbow>
 __global__ __launch_bounds__(kThreads) void pair_count_reduce_kernel(const int32_t *__restrict__ len,
                                                                      int64_t n, int32_t width,
                                                                      int32_t window,
@@ -62,7 +76,7 @@ __global__ __launch_bounds__(kThreads) void pair_count_reduce_kernel(const int32
 #pragma unroll 4
   for (int i = 0; i < kItems; ++i) {
     const int64_t r = base + int64_t(i) * kThreads + threadIdx.x;
-    if (r < n) s += walk_pairs(clamped_len(len, r, width, bad), window);
+    if (r < n) s += walk_items<kCbow>(clamped_len(len, r, width, bad), window);
   }
   const int64_t total = block_sum<kThreads, int64_t>(s, scratch);
   if (threadIdx.x == 0) partials[blockIdx.x] = total;
@@ -88,6 +102,7 @@ __global__ __launch_bounds__(kThreads) void pair_partials_kernel(int64_t *partia
   }
 }
 
+template <bool kCbow>
 __global__ __launch_bounds__(kThreads) void pair_offsets_kernel(const int32_t *__restrict__ len, int64_t n,
                                                                 int32_t width, int32_t window,
                                                                 const int64_t *__restrict__ partials,
@@ -98,7 +113,7 @@ __global__ __launch_bounds__(kThreads) void pair_offsets_kernel(const int32_t *_
   int bad = 0;
   for (int i = 0; i < kItems; ++i) {
     const int64_t r = base + int64_t(i) * kThreads + threadIdx.x;
-    const int64_t x = r < n ? walk_pairs(clamped_len(len, r, width, bad), window) : 0;
+    const int64_t x = r < n ? walk_items<kCbow>(clamped_len(len, r, width, bad), window) : 0;
     int64_t tot;
     const int64_t ex = block_exclusive_scan<kThreads, int64_t>(x, scratch, tot);
     if (r < n) offsets[r] = carry + ex;
@@ -198,6 +213,91 @@ __global__ __launch_bounds__(kBlock) void pair_emit_kernel(const int32_t *__rest
     atomicOr(status, (full ? RDF2V_STATUS_CAPACITY : 0) | (bad ? RDF2V_STATUS_BAD_LENGTH : 0));
 }
 
+// Streams `total` int32 from LDS to dst (4-byte aligned) with the whole block:
+// a scalar head up to 16-byte alignment, 16-byte non-temporal stores, a scalar
+// tail.
+template <int kBlock>
+__device__ __forceinline__ void stream_run(const int32_t *src, int32_t *dst, int64_t total) {
+  const int t = threadIdx.x;
+  const int64_t head = min(total, int64_t((16 - (reinterpret_cast<uintptr_t>(dst) & 15)) & 15) / 4);
+  if (t < head) __builtin_nontemporal_store(src[t], dst + t);
+  const int64_t body = (total - head) >> 2;
+  v4i32 *dst4 = reinterpret_cast<v4i32 *>(dst + head);
+  for (int64_t q = t; q < body; q += kBlock) {
+    const int32_t *s4 = src + head + 4 * q;
+    __builtin_nontemporal_store(v4i32{s4[0], s4[1], s4[2], s4[3]}, dst4 + q);
+  }
+  for (int64_t q = head + 4 * body + t; q < total; q += kBlock) __builtin_nontemporal_store(src[q], dst + q);
+}
+
+// CBOW: one thread per (walk, position); walks_per_block = kBlock / width
+// walks per block, whose examples form one contiguous output range. With
+// kStage, the block copies its rows to LDS, places its centers and context rows
+// in LDS stages (at most kBlock examples, 2 * window ints per context row) and
+// streams each out as one contiguous run of 16-byte non-temporal stores;
+// otherwise each thread writes its own center and context row.
+template <bool kStage, int kBlock>
+__global__ __launch_bounds__(kBlock) void cbow_emit_kernel(const int32_t *__restrict__ tokens,
+                                                            const int32_t *__restrict__ len, int64_t n,
+                                                            int32_t width, int32_t window,
+                                                            const int64_t *__restrict__ offsets,
+                                                            int32_t *__restrict__ centers,
+                                                            int32_t *__restrict__ contexts, int64_t capacity,
+                                                            int32_t *status) {
+  extern __shared__ int32_t ctx_stage[];              // kStage: the block's context rows
+  __shared__ int32_t rows[kStage ? kBlock : 1];       // the block's walk rows
+  __shared__ int32_t ctr_stage[kStage ? kBlock : 1];  // kStage: the block's centers
+  const int walks_per_block = kBlock / width;
+  const int t = threadIdx.x;
+  const int64_t r0 = int64_t(blockIdx.x) * walks_per_block;
+  const int64_t r_end = min(n, r0 + walks_per_block);
+  const int64_t r = r0 + t / width;
+  const int64_t i = t % width;
+  const bool active = t < walks_per_block * width && r < n;
+  const int64_t cw = 2 * int64_t(window);  // context entries per example
+  int bad = 0;
+  const int64_t block_first = offsets[r0];
+  int64_t L = 0;
+  if (active) L = clamped_len(len, r, width, bad);
+  if (kStage) {
+    const int64_t span = (r_end - r0) * width;  // <= kBlock
+    if (t < span) rows[t] = tokens[r0 * width + t];
+    __syncthreads();
+  }
+  bool full = false;
+  if (active && i < L) {
+    const int32_t *row = kStage ? rows + (t / width) * width : tokens + r * width;
+    const int64_t e = offsets[r] + i;
+    if (e >= capacity) full = true;
+    if (kStage) ctr_stage[e - block_first] = row[i];
+    else if (e < capacity) centers[e] = row[i];
+    int32_t *ctx = kStage ? ctx_stage + (e - block_first) * cw : contexts + e * cw;
+    if (kStage || e < capacity) {
+      const int64_t j0 = max(int64_t(0), i - window), j1 = min(L - 1, i + int64_t(window));
+      int64_t m = 0;
+      for (int64_t j = j0; j <= j1; ++j)
+        if (j != i) ctx[m++] = row[j];
+      for (; m < cw; ++m) ctx[m] = -1;
+    }
+  }
+  if (kStage) {
+    __syncthreads();
+    // The block's examples end where the next block's begin.
+    int64_t block_end;
+    if (r_end < n) {
+      block_end = offsets[r_end];
+    } else {
+      int b2 = 0;
+      block_end = offsets[n - 1] + clamped_len(len, n - 1, width, b2);
+    }
+    const int64_t lim = max(int64_t(0), min(block_end, capacity) - block_first);  // examples that fit
+    stream_run<kBlock>(ctr_stage, centers + block_first, lim);
+    stream_run<kBlock>(ctx_stage, contexts + block_first * cw, lim * cw);
+  }
+  if ((full || bad) && status != nullptr)
+    atomicOr(status, (full ? RDF2V_STATUS_CAPACITY : 0) | (bad ? RDF2V_STATUS_BAD_LENGTH : 0));
+}
+
 constexpr size_t kMaxStageBytes = 32 << 10;
 
 // Most pairs one walk of this width can give.
@@ -224,15 +324,16 @@ rdf2v_status launch_skipgram_pairs(const int32_t *tokens, const int32_t *len, in
   int64_t *partials = reinterpret_cast<int64_t *>(ws + align_up(size_t(num_walks) * 8, 256));
   const int64_t nb = ceil_div(num_walks, kTile);
   if (nb > 0) {
-    pair_count_reduce_kernel<<<dim3(unsigned(nb)), dim3(kThreads), 0, stream>>>(len, num_walks, width, window,
-                                                                               partials, status_dev);
+    pair_count_reduce_kernel<false><<<dim3(unsigned(nb)), dim3(kThreads), 0, stream>>>(len, num_walks, width,
+                                                                                      window, partials,
+                                                                                      status_dev);
     RDF2V_LAUNCH_CHECK();
   }
   pair_partials_kernel<<<dim3(1), dim3(kThreads), 0, stream>>>(partials, nb, count_out);
   RDF2V_LAUNCH_CHECK();
   if (nb == 0) return RDF2V_OK;
-  pair_offsets_kernel<<<dim3(unsigned(nb)), dim3(kThreads), 0, stream>>>(len, num_walks, width, window,
-                                                                        partials, offsets);
+  pair_offsets_kernel<false><<<dim3(unsigned(nb)), dim3(kThreads), 0, stream>>>(len, num_walks, width, window,
+                                                                               partials, offsets);
   RDF2V_LAUNCH_CHECK();
   if (capacity > 0) {
     int2 *out = reinterpret_cast<int2 *>(pairs_out);
@@ -259,6 +360,47 @@ rdf2v_status launch_skipgram_pairs(const int32_t *tokens, const int32_t *len, in
     return launch(pair_emit_kernel<false, kThreads>, kThreads, 0);
   }
   return RDF2V_OK;
+}
+
+rdf2v_status launch_cbow_examples(const int32_t *tokens, const int32_t *len, int64_t num_walks, int32_t width,
+                                  int32_t window, int32_t *centers_out, int32_t *contexts_out, int64_t capacity,
+                                  int64_t *count_out, void *workspace, int32_t *status_dev, hipStream_t stream) {
+  char *ws = static_cast<char *>(workspace);
+  int64_t *offsets = reinterpret_cast<int64_t *>(ws);
+  int64_t *partials = reinterpret_cast<int64_t *>(ws + align_up(size_t(num_walks) * 8, 256));
+  const int64_t nb = ceil_div(num_walks, kTile);
+  if (nb > 0) {
+    pair_count_reduce_kernel<true><<<dim3(unsigned(nb)), dim3(kThreads), 0, stream>>>(len, num_walks, width, window,
+                                                                                     partials, status_dev);
+    RDF2V_LAUNCH_CHECK();
+  }
+  pair_partials_kernel<<<dim3(1), dim3(kThreads), 0, stream>>>(partials, nb, count_out);
+  RDF2V_LAUNCH_CHECK();
+  if (nb == 0) return RDF2V_OK;
+  pair_offsets_kernel<true><<<dim3(unsigned(nb)), dim3(kThreads), 0, stream>>>(len, num_walks, width, window,
+                                                                              partials, offsets);
+  RDF2V_LAUNCH_CHECK();
+  if (capacity == 0) return RDF2V_OK;
+  // A block of B threads holds at most B examples, so its stage is B rows of
+  // 2 * window ints: 256-thread blocks up to 32 KB, else 128 or 64, else direct
+  // stores. (Measured at window 5 on 48.9M walks: 512-thread blocks, or two or
+  // four positions per thread, were 2-50 % slower.)
+  const size_t row_bytes = size_t(2) * size_t(window) * sizeof(int32_t);
+  auto launch = [&](auto kernel, int block, size_t lds) -> rdf2v_status {
+    const int64_t blocks = ceil_div(num_walks, block / width);
+    if (blocks >= (int64_t(1) << 31)) return RDF2V_ERR_TOO_LARGE;
+    kernel<<<dim3(unsigned(blocks)), dim3(block), lds, stream>>>(tokens, len, num_walks, width, window, offsets,
+                                                                 centers_out, contexts_out, capacity, status_dev);
+    RDF2V_LAUNCH_CHECK();
+    return RDF2V_OK;
+  };
+  if (width <= 256 && 256 * row_bytes <= kMaxStageBytes)
+    return launch(cbow_emit_kernel<true, 256>, 256, 256 * row_bytes);
+  if (width <= 128 && 128 * row_bytes <= kMaxStageBytes)
+    return launch(cbow_emit_kernel<true, 128>, 128, 128 * row_bytes);
+  if (width <= 64 && 64 * row_bytes <= kMaxStageBytes)
+    return launch(cbow_emit_kernel<true, 64>, 64, 64 * row_bytes);
+  return launch(cbow_emit_kernel<false, kThreads>, kThreads, 0);
 }
 
 }  // namespace rdf2v

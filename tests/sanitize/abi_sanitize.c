@@ -36,6 +36,7 @@ int main(void) {
       for (size_t k = 0; k < n64; ++k) sink += rdf2v_build_vocabulary_workspace_size(big64[i], big64[k], big64[k]);
     }
     sink += rdf2v_skipgram_pairs_workspace_size(big64[i]);
+    sink += rdf2v_cbow_examples_workspace_size(big64[i]);
     sink += rdf2v_unique_walks_workspace_size(big64[i]);
   }
   for (size_t j = 0; j < n32; ++j) sink += rdf2v_nonsink_starts_workspace_size(big32[j]);
@@ -67,6 +68,12 @@ int main(void) {
   EXPECT(rdf2v_skipgram_pairs(FI, FI, INT64_MAX, 129, 5, FI, 1, (int64_t *)F, F, 1 << 20, NULL, NULL) ==
          RDF2V_ERR_TOO_LARGE);
   EXPECT(rdf2v_skipgram_pairs(FI, FI, 10, 0, 5, FI, 1, (int64_t *)F, F, 1 << 20, NULL, NULL) ==
+         RDF2V_ERR_INVALID_ARGUMENT);
+  EXPECT(rdf2v_cbow_examples(FI, FI, INT64_MAX, 129, 5, FI, FI, 1, (int64_t *)F, F, 1 << 20, NULL, NULL) ==
+         RDF2V_ERR_TOO_LARGE);
+  EXPECT(rdf2v_cbow_examples(FI, FI, 10, 9, 5, FI, FI, INT64_MAX, (int64_t *)F, F, 1 << 20, NULL, NULL) ==
+         RDF2V_ERR_TOO_LARGE);
+  EXPECT(rdf2v_cbow_examples(FI, FI, 10, 9, 0, FI, FI, 1, (int64_t *)F, F, 1 << 20, NULL, NULL) ==
          RDF2V_ERR_INVALID_ARGUMENT);
   EXPECT(rdf2v_unique_walks(FI, FI, INT64_MAX, 3, INT32_MAX, FI, FI, (int64_t *)F, F, 1 << 20, NULL, NULL) ==
          RDF2V_ERR_TOO_LARGE);

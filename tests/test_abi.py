@@ -35,7 +35,8 @@ def test_header_declares_the_calls():
               "rdf2v_skipgram_pairs", "rdf2v_skipgram_pairs_workspace_size", "rdf2v_random_walks_tokens",
               "rdf2v_unique_walks", "rdf2v_unique_walks_workspace_size", "rdf2v_bfs_walks",
               "rdf2v_bfs_walks_workspace_size", "rdf2v_build_vocabulary",
-              "rdf2v_build_vocabulary_workspace_size", "rdf2v_walk_edges_recommended"]:
+              "rdf2v_build_vocabulary_workspace_size", "rdf2v_walk_edges_recommended",
+              "rdf2v_cbow_examples", "rdf2v_cbow_examples_workspace_size"]:
         assert n in names
 
 
@@ -197,6 +198,39 @@ def test_skipgram_argument_validation(lib):
     assert call(wsb=need - 1) == pkg.RDF2V_ERR_WORKSPACE
     assert pkg.rdf2v_skipgram_pairs_workspace_size(0) > 0
     assert pkg.rdf2v_skipgram_pairs_workspace_size(10**6) >= 8 * 10**6
+
+
+def test_cbow_argument_validation(lib):
+    so, pkg = lib
+    f = so.rdf2v_cbow_examples
+    need = pkg.rdf2v_cbow_examples_workspace_size(100)
+    WS = ctypes.c_void_p(1 << 41)
+    E_INV = pkg.RDF2V_ERR_INVALID_ARGUMENT
+    ok_args = dict(tokens=FAKE, len=FAKE, n=100, width=9, window=5, centers=FAKE, contexts=FAKE8, cap=10,
+                   count=FAKE, ws=WS, wsb=need)
+
+    def call(**kw):
+        a = dict(ok_args, **kw)
+        return f(a["tokens"], a["len"], a["n"], a["width"], a["window"], a["centers"], a["contexts"], a["cap"],
+                 a["count"], a["ws"], a["wsb"], None, None)
+
+    assert call(n=-1) == E_INV
+    assert call(window=0) == E_INV
+    assert call(window=129) == E_INV
+    assert call(cap=-1) == E_INV
+    assert call(width=0) == E_INV
+    assert call(width=130) == E_INV
+    assert call(count=None) == E_INV
+    assert call(tokens=None) == E_INV
+    assert call(len=None) == E_INV
+    assert call(centers=None) == E_INV
+    assert call(contexts=None) == E_INV
+    assert call(contexts=ctypes.c_void_p((1 << 40) + 2)) == E_INV
+    assert call(n=2**47) == pkg.RDF2V_ERR_TOO_LARGE
+    assert call(ws=None) == pkg.RDF2V_ERR_WORKSPACE
+    assert call(wsb=need - 1) == pkg.RDF2V_ERR_WORKSPACE
+    assert pkg.rdf2v_cbow_examples_workspace_size(10**6) >= 8 * 10**6
+    assert pkg.rdf2v_cbow_examples_workspace_size(2**47) == 0
 
 
 def test_token_kind_and_unique_validation(lib):
