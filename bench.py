@@ -31,7 +31,7 @@ METRIC = "walk tokens/sec on 1 MI355X + achieved HBM GB/s fraction of peak"
 HBM_PEAK_GBS = 8000.0
 PMC_FILE = os.path.join(ROOT, "profiles", "walk_kernel_pmc.json")
 WALK_SOURCES = [os.path.join(ROOT, "paper_2508_01073_amd", "csrc", f)
-                for f in ("random_walk.hip", "common.hpp", "launch.hpp")]
+                for f in ("random_walk.hip", "common.hpp", "walk.hpp")]
 
 
 def kernel_source_hash() -> str:

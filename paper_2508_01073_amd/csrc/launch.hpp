@@ -8,6 +8,7 @@
 #include <cstdint>
 
 #include "rdf2v.h"
+#include "walk.hpp"
 
 namespace rdf2v {
 
@@ -31,31 +32,6 @@ rdf2v_status launch_csr_build(const int32_t *subj, const int32_t *pred, const in
 size_t nonsink_workspace_bytes(int32_t num_entities);
 rdf2v_status launch_nonsink_starts(const int32_t *row_ptr, int32_t num_entities, int32_t *starts_out,
                                    int64_t *count_out, void *workspace, hipStream_t stream);
-
-struct WalkArgs {
-  const int32_t *row_ptr;
-  const int32_t *edges;       // (predicate, object) pairs, 8-byte aligned
-  const int32_t *walk_edges;  // optional (predicate, object, row lo, row hi), 16-byte aligned
-  const int32_t *start;
-  int32_t *tokens;
-  int32_t *lens;
-  int32_t *status;
-  int64_t walk_begin;
-  int64_t walk_count;
-  int64_t num_edges;
-  int32_t num_entities;
-  int32_t num_predicates;
-  int32_t walks_per_node;
-  int32_t depth;
-  int32_t token_kind;  // rdf2v_walk_tokens
-  uint32_t key_lo;
-  uint32_t key_hi;
-};
-rdf2v_status launch_random_walks(const WalkArgs &args, hipStream_t stream);
-
-rdf2v_status launch_walk_edges(const int32_t *row_ptr, const int32_t *edges, int64_t num_edges,
-                               int32_t num_entities, int32_t *walk_edges_out, int32_t *status_dev,
-                               hipStream_t stream);
 
 size_t skipgram_workspace_bytes(int64_t num_walks);
 rdf2v_status launch_cbow_examples(const int32_t *tokens, const int32_t *len, int64_t num_walks, int32_t width,

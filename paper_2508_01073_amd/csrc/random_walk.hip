@@ -24,7 +24,7 @@
 // CSR or an out-of-range id raises a status bit instead of faulting.
 
 #include "common.hpp"
-#include "launch.hpp"
+#include "walk.hpp"
 
 namespace rdf2v {
 namespace {
