@@ -16,6 +16,7 @@ import paper_2508_01073_amd as rd
 import synth
 from gpu_helpers import (assert_csr_equal, assert_rows_equal, assert_walk_records, check_walk_properties,
                          compare_all, compare_windows, device, gpu_csr, gpu_walks, new_status, plain, say, to_dev)
+from sparse_ids import expected_on_sparse, sparse_graph
 
 pytestmark = pytest.mark.gpu
 
@@ -297,6 +298,36 @@ def test_walk_ids_beyond_2_pow_32():
         for c, what in [(csr, "walk records"), (plain(csr), "plain records")]:
             tok, ln = gpu_walks(c, to_dev(starts), wpn, 9, 42, b, 1000)
             assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr_, lr_, f"walks from {b} {what}")
+
+
+def test_largest_id_space():
+    # V + P = 2^31 - 1, the largest id space the token layout allows: 31-bit subject keys (four
+    # 8-bit radix passes), an 8 GiB row_ptr, start-set scans over 2^31 entities, and the token
+    # V + P - 1 = 2^31 - 2. The expectation is the oracle's on the compact graph, relabelled
+    # (sparse_ids; the relabel is checked against the oracle itself on the CPU).
+    P = 7
+    V = 2**31 - 1 - P
+    wpn, depth = 3, 6
+    say(f"[edge] largest id space V={V} P={P}: CSR, walk records, start set, walks")
+    U, s_r, p, o_r = sparse_graph(V, P, 300_000, 20_000, seed=31)
+    rp_x, ed_x, starts_x, tok_x, ln_x = expected_on_sparse(U, s_r, p, o_r, V, P, wpn, depth, 42)
+    assert int(tok_x.max()) == 2**31 - 2
+    csr = gpu_csr(U[s_r], p, U[o_r], V, P)
+    ed = csr.edges.cpu().numpy()
+    assert np.array_equal(ed, ed_x), "edge records differ"
+    chunk = 1 << 28
+    for a in range(0, V + 1, chunk):
+        got = csr.row_ptr[a:a + chunk].cpu().numpy()
+        assert np.array_equal(got, rp_x[a:a + chunk]), f"row_ptr differs in [{a}, {a + chunk})"
+    assert rd.rdf2v_walk_edges_recommended(V, csr.num_edges)
+    csr_r = rd.rdf2v_build_walk_edges(csr)
+    torch.cuda.synchronize()
+    assert_walk_records(csr_r, rp_x, ed_x)
+    starts = rd.rdf2v_nonsink_starts(csr)
+    assert np.array_equal(starts.cpu().numpy(), starts_x)
+    for c, what in [(csr_r, "walk records"), (csr, "plain records")]:
+        tok, ln = gpu_walks(c, starts, wpn, depth, 42)
+        assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tok_x, ln_x, f"largest id space, {what}")
 
 
 def test_concurrent_streams_do_not_interfere():
