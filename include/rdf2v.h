@@ -155,7 +155,8 @@ size_t rdf2v_nonsink_starts_workspace_size(int32_t num_entities);
  *   starts_out  [num_entities] int32 (device): the first *count_out entries
  *               are written.
  *   count_out   one int64 in device memory: the number of start entities.
- *   workspace   device scratch, rdf2v_nonsink_starts_workspace_size() bytes.
+ *   workspace   device scratch, rdf2v_nonsink_starts_workspace_size() bytes,
+ *               256-byte aligned.
  */
 rdf2v_status rdf2v_nonsink_starts(const rdf2v_csr *csr, int32_t *starts_out, int64_t *count_out,
                                   void *workspace, size_t workspace_bytes, void *stream);

@@ -85,6 +85,7 @@ RDF2V_API rdf2v_status rdf2v_nonsink_starts(const rdf2v_csr *csr, int32_t *start
   if (csr->num_entities > 0 && starts_out == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
   const size_t need = rdf2v::nonsink_workspace_bytes(csr->num_entities);
   if (workspace == nullptr || workspace_bytes < need) return RDF2V_ERR_WORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return RDF2V_ERR_WORKSPACE;
   return rdf2v::launch_nonsink_starts(csr->row_ptr, csr->num_entities, starts_out, count_out,
                                       workspace, static_cast<hipStream_t>(stream));
 }

@@ -321,6 +321,7 @@ def test_nonsink_argument_validation(lib):
     assert f(ctypes.byref(c), None, FAKE, FAKE, need, None) == pkg.RDF2V_ERR_INVALID_ARGUMENT
     assert f(ctypes.byref(c), FAKE, FAKE, None, need, None) == pkg.RDF2V_ERR_WORKSPACE
     assert f(ctypes.byref(c), FAKE, FAKE, FAKE, need - 1, None) == pkg.RDF2V_ERR_WORKSPACE
+    assert f(ctypes.byref(c), FAKE, FAKE, ctypes.c_void_p((1 << 41) + 4), need, None) == pkg.RDF2V_ERR_WORKSPACE
 
 
 def test_binding_has_no_cpu_fallback(lib):
