@@ -143,6 +143,31 @@ def _dev_i32(t: torch.Tensor, name: str) -> torch.Tensor:
     return t
 
 
+def _out(t: torch.Tensor, name: str, dtype: torch.dtype, min_numel: int, dev: torch.device) -> torch.Tensor:
+    """A caller-supplied output: on the call's device, of the given dtype, contiguous, and large
+    enough (the library writes through the raw pointer, so a short buffer would be overrun)."""
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or t.device != dev:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor on {dev}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < min_numel:
+        raise ValueError(f"{name} holds {t.numel()} elements; this call needs {min_numel}")
+    return t
+
+
+def _status(t: torch.Tensor | None, dev: torch.device) -> torch.Tensor | None:
+    """The optional device status word (one int32 the kernels OR error bits into)."""
+    return None if t is None else _out(t, "status", torch.int32, 1, dev)
+
+
+def _same_device(dev: torch.device, **tensors) -> None:
+    for name, t in tensors.items():
+        if t is not None and t.device != dev:
+            raise TypeError(f"{name} must be on {dev}, got {t.device}")
+
+
 def _ws_bytes(t: torch.Tensor | None) -> int:
     """Size in bytes of a caller workspace (any dtype; contiguous device memory)."""
     if t is None:
@@ -200,10 +225,14 @@ def rdf2v_build_csr(subj: torch.Tensor, pred: torch.Tensor, obj: torch.Tensor, n
     if pred.shape[0] != t or obj.shape[0] != t:
         raise ValueError("subj, pred and obj differ in length")
     dev = subj.device
+    _same_device(dev, pred=pred, obj=obj)
     if row_ptr is None:
         row_ptr = torch.empty(num_entities + 1, dtype=torch.int32, device=dev)
     if edges is None:
         edges = torch.empty((t, 2), dtype=torch.int32, device=dev)
+    _out(row_ptr, "row_ptr", torch.int32, num_entities + 1, dev)
+    _out(edges, "edges", torch.int32, 2 * t, dev)
+    _status(status, dev)
     need = rdf2v_build_csr_workspace_size(t, num_entities)
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
@@ -222,8 +251,9 @@ def rdf2v_build_walk_edges(csr: Csr, *, out: torch.Tensor | None = None,
     dev = csr.row_ptr.device
     if out is None:
         out = torch.empty((csr.num_edges, 4), dtype=torch.int32, device=dev)
-    if out.numel() < 4 * csr.num_edges:
-        raise ValueError("out too small for num_edges walk records")
+    _same_device(dev, edges=csr.edges)
+    _out(out, "out", torch.int32, 4 * csr.num_edges, dev)
+    _status(status, dev)
     c = csr._c()
     st = _native().rdf2v_build_walk_edges(ctypes.byref(c), _ptr(out), _ptr(status), _stream(dev, stream))
     _check(st, "rdf2v_build_walk_edges")
@@ -253,6 +283,8 @@ def rdf2v_nonsink_starts(csr: Csr, *, workspace: torch.Tensor | None = None, str
     if workspace is None:
         workspace = torch.empty(rdf2v_nonsink_starts_workspace_size(csr.num_entities),
                                 dtype=torch.uint8, device=dev)
+    _out(starts, "starts", torch.int32, csr.num_entities, dev)
+    _out(count, "count", torch.int64, 1, dev)
     c = csr._c()
     st = _native().rdf2v_nonsink_starts(ctypes.byref(c), _ptr(starts), _ptr(count), _ptr(workspace),
                                    _ws_bytes(workspace), _stream(dev, stream))
@@ -295,8 +327,11 @@ def _walks(csr, start_nodes, walks_per_node, depth, seed, walk_begin, walk_count
         tokens = torch.empty((max(walk_count, 0), max(width, 1)), dtype=torch.int32, device=dev)
     if lens is None:
         lens = torch.empty(max(walk_count, 0), dtype=torch.int32, device=dev)
-    if walk_count > 0 and (tokens.numel() < walk_count * width or lens.numel() < walk_count):
-        raise ValueError("output buffers too small for walk_count rows")
+    rows = max(walk_count, 0)
+    _out(tokens, "tokens", torch.int32, rows * width, dev)
+    _out(lens, "lens", torch.int32, rows, dev)
+    _status(status, dev)
+    _same_device(dev, row_ptr=csr.row_ptr, edges=csr.edges, walk_edges=csr.walk_edges)
     c = csr._c()
     st = _native().rdf2v_random_walks_tokens(ctypes.byref(c), _ptr(start_nodes), start_nodes.shape[0],
                                              walks_per_node, depth, ctypes.c_uint64(seed & (2**64 - 1)),
@@ -329,6 +364,11 @@ def rdf2v_unique_walks(tokens: torch.Tensor, lens: torch.Tensor, group_size: int
         count = torch.empty(1, dtype=torch.int64, device=dev)
     if workspace is None:
         workspace = torch.empty(max(rdf2v_unique_walks_workspace_size(n), 1), dtype=torch.uint8, device=dev)
+    _same_device(dev, lens=lens)
+    _out(tokens_out, "tokens_out", torch.int32, n * width, dev)
+    _out(lens_out, "lens_out", torch.int32, n, dev)
+    _out(count, "count", torch.int64, 1, dev)
+    _status(status, dev)
     st = _native().rdf2v_unique_walks(_ptr(tokens), _ptr(lens), n, group_size, width, _ptr(tokens_out),
                                       _ptr(lens_out), _ptr(count), _ptr(workspace), _ws_bytes(workspace),
                                       _ptr(status), _stream(dev, stream))
@@ -362,6 +402,11 @@ def rdf2v_bfs_walks(csr: Csr, roots: torch.Tensor, depth: int, max_walks: int, *
     if workspace is None:
         workspace = torch.empty(max(rdf2v_bfs_walks_workspace_size(csr.num_entities, R), 1),
                                 dtype=torch.uint8, device=dev)
+    _same_device(dev, row_ptr=csr.row_ptr, edges=csr.edges)
+    _out(tokens, "tokens", torch.int32, R * max(max_walks, 0) * width, dev)
+    _out(lens, "lens", torch.int32, R * max(max_walks, 0), dev)
+    _out(counts, "counts", torch.int32, R, dev)
+    _status(status, dev)
     c = csr._c()
     st = _native().rdf2v_bfs_walks(ctypes.byref(c), _ptr(roots), R, depth, max_walks, _ptr(tokens), _ptr(lens),
                                    _ptr(counts), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
@@ -391,6 +436,9 @@ def rdf2v_skipgram_pairs(tokens: torch.Tensor, lens: torch.Tensor, window: int, 
         workspace = torch.empty(max(rdf2v_skipgram_pairs_workspace_size(w), 1), dtype=torch.uint8, device=dev)
     if count is None:
         count = torch.empty(1, dtype=torch.int64, device=dev)
+    _same_device(dev, lens=lens)
+    _out(count, "count", torch.int64, 1, dev)
+    _status(status, dev)
 
     def call(out, cap):
         st = _native().rdf2v_skipgram_pairs(_ptr(tokens), _ptr(lens), w, width, window, _ptr(out), cap,
@@ -399,6 +447,9 @@ def rdf2v_skipgram_pairs(tokens: torch.Tensor, lens: torch.Tensor, window: int, 
         _check(st, "rdf2v_skipgram_pairs")
 
     if pairs is not None:
+        if pairs.dim() != 2 or pairs.shape[1] != 2:
+            raise ValueError("pairs must have shape [capacity, 2]")
+        _out(pairs, "pairs", torch.int32, 0, dev)
         call(pairs, int(pairs.shape[0]))
         return pairs, count
     call(None, 0)
@@ -431,6 +482,9 @@ def rdf2v_cbow_examples(tokens: torch.Tensor, lens: torch.Tensor, window: int, *
         workspace = torch.empty(max(rdf2v_cbow_examples_workspace_size(w), 1), dtype=torch.uint8, device=dev)
     if count is None:
         count = torch.empty(1, dtype=torch.int64, device=dev)
+    _same_device(dev, lens=lens)
+    _out(count, "count", torch.int64, 1, dev)
+    _status(status, dev)
 
     def call(c, x, cap):
         st = _native().rdf2v_cbow_examples(_ptr(tokens), _ptr(lens), w, width, window, _ptr(c), _ptr(x), cap,
@@ -441,10 +495,9 @@ def rdf2v_cbow_examples(tokens: torch.Tensor, lens: torch.Tensor, window: int, *
     if (centers is None) != (contexts is None):
         raise ValueError("give both centers and contexts, or neither")
     if centers is not None:
-        _dev_i32(centers, "centers"); _dev_i32(contexts, "contexts")
-        cap = int(centers.shape[0])
-        if contexts.numel() < cap * 2 * window:
-            raise ValueError("contexts must hold 2 * window entries per center")
+        cap = int(centers.numel())
+        _out(centers, "centers", torch.int32, 0, dev)
+        _out(contexts, "contexts", torch.int32, cap * 2 * max(window, 0), dev)
         call(centers, contexts, cap)
         return centers, contexts, count
     call(None, None, 0)
@@ -487,9 +540,11 @@ def rdf2v_build_vocabulary(subj, pred, obj, max_entities: int, max_predicates: i
     if ids is None:
         ids = tuple(torch.empty(n, dtype=torch.int32, device=dev) for _ in range(3))
     for i, name in zip(ids, ("subj_ids", "pred_ids", "obj_ids")):
-        _dev_i32(i, name)
+        _out(i, name, torch.int32, n, dev)
     if counts is None:
         counts = torch.empty(2, dtype=torch.int64, device=dev)
+    _out(counts, "counts", torch.int64, 2, dev)
+    _status(status, dev)
     if workspace is None:
         need = rdf2v_build_vocabulary_workspace_size(n, max_entities, max_predicates)
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)

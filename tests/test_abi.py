@@ -333,3 +333,16 @@ def test_binding_has_no_cpu_fallback(lib):
                 text = open(os.path.join(dirpath, fn)).read()
                 assert "import oracle" not in text and "from oracle" not in text, fn
                 assert "rdf2v_oracle" not in text and "rdf2v_ref_" not in text, fn
+
+
+def test_binding_rejects_host_outputs():
+    # Caller-supplied outputs and the status word must be device tensors of the right dtype and
+    # size: the library writes through raw pointers. (Device-side cases: test_gpu_binding.py.)
+    import paper_2508_01073_amd as rd
+    import torch
+    dev = torch.device("cuda", 0)
+    with pytest.raises(TypeError):
+        rd._out(torch.zeros(4, dtype=torch.int32), "x", torch.int32, 4, dev)
+    with pytest.raises(TypeError):
+        rd._status(torch.zeros(1, dtype=torch.int32), dev)
+    assert rd._status(None, dev) is None
