@@ -15,7 +15,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "librdf2v.so")
-SOURCES = ["api.hip", "csr_build.hip", "random_walk.hip", "skipgram.hip", "unique_walks.hip", "bfs_walks.hip",
+SOURCES = ["api.hip", "csr_build.hip", "random_walk.hip", "walk_edges.hip", "skipgram.hip", "unique_walks.hip", "bfs_walks.hip",
            "vocab.hip"]
 ARCH = "gfx950"
 

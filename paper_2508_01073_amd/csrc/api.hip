@@ -61,6 +61,8 @@ RDF2V_API rdf2v_status rdf2v_build_walk_edges(const rdf2v_csr *csr, int32_t *wal
     return RDF2V_ERR_TOO_LARGE;
   if (csr->num_edges == 0) return RDF2V_OK;
   if (csr->edges == nullptr || walk_edges_out == nullptr) return RDF2V_ERR_INVALID_ARGUMENT;
+  // Every object must be < num_entities; with no entities that is impossible.
+  if (csr->num_entities == 0) return RDF2V_ERR_ID_OUT_OF_RANGE;
   if ((reinterpret_cast<uintptr_t>(csr->edges) & 7) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
   if ((reinterpret_cast<uintptr_t>(walk_edges_out) & 15) != 0) return RDF2V_ERR_INVALID_ARGUMENT;
   return rdf2v::launch_walk_edges(csr->row_ptr, csr->edges, csr->num_edges, csr->num_entities,

@@ -30,7 +30,6 @@ namespace rdf2v {
 namespace {
 
 typedef int32_t v4i32 __attribute__((ext_vector_type(4)));
-typedef int32_t v2i32 __attribute__((ext_vector_type(2)));
 
 // Philox4x32-10 (Salmon, Moraes, Dror & Shaw, SC'11): ten rounds of two
 // 32x32->64-bit products of counter words 0 and 2 with the Philox multipliers,
@@ -168,49 +167,6 @@ __global__ __launch_bounds__(kBlock) void random_walk_kernel(const WalkArgs a) {
   if (flags != 0 && a.status != nullptr) atomicOr(a.status, flags);
 }
 
-// walk_edges[k] = (pred, obj, row_ptr[obj], row_ptr[obj + 1]) for record k.
-// Each thread handles kWalkEdgeItems records strided by the block size, issuing
-// all loads, then all row-bound gathers, then all stores, so that several
-// independent memory operations per lane are in flight.
-constexpr int kWalkEdgeThreads = 256;
-constexpr int kWalkEdgeItems = 4;
-constexpr int kWalkEdgeTile = kWalkEdgeThreads * kWalkEdgeItems;
-
-__global__ __launch_bounds__(kWalkEdgeThreads) void walk_edges_kernel(
-    const int32_t *__restrict__ row_ptr, const int2 *__restrict__ edges, int64_t n,
-    int32_t num_entities, v4i32 *__restrict__ out, int32_t *status) {
-  const int64_t base = int64_t(blockIdx.x) * kWalkEdgeTile + threadIdx.x;
-  int2 rec[kWalkEdgeItems];
-  int2 bounds[kWalkEdgeItems];
-  int bad = 0;
-#pragma unroll
-  for (int j = 0; j < kWalkEdgeItems; ++j) {
-    const int64_t i = base + j * kWalkEdgeThreads;
-    rec[j] = make_int2(0, 0);
-    if (i < n) {
-      // streamed once: non-temporal, so the row_ptr lines gathered below stay in L2
-      const v2i32 v = __builtin_nontemporal_load(reinterpret_cast<const v2i32 *>(edges) + i);
-      rec[j] = make_int2(v.x, v.y);
-    }
-  }
-  // The gathers of all items are issued together: an object id out of range is
-  // flagged and read as entity 0, so no load waits on a branch.
-#pragma unroll
-  for (int j = 0; j < kWalkEdgeItems; ++j) {
-    const int64_t i = base + j * kWalkEdgeThreads;
-    const bool ok = uint32_t(rec[j].y) < uint32_t(num_entities);
-    const int32_t o = ok ? rec[j].y : 0;
-    bad |= (i < n && !ok) ? 1 : 0;
-    bounds[j] = i < n ? make_int2(row_ptr[o], row_ptr[o + 1]) : make_int2(0, 0);
-  }
-#pragma unroll
-  for (int j = 0; j < kWalkEdgeItems; ++j) {
-    const int64_t i = base + j * kWalkEdgeThreads;
-    if (i < n) __builtin_nontemporal_store(v4i32{rec[j].x, rec[j].y, bounds[j].x, bounds[j].y}, out + i);
-  }
-  if (bad && status != nullptr) atomicOr(status, RDF2V_STATUS_ID_OUT_OF_RANGE);
-}
-
 template <int kBlock, int kKind>
 void launch_kind(const WalkArgs &a, int64_t blocks, size_t lds, hipStream_t stream) {
   if (a.walk_edges != nullptr)
@@ -241,18 +197,6 @@ rdf2v_status launch_random_walks(const WalkArgs &a, hipStream_t stream) {
   // The LDS tile holds kBlock rows of 2*depth+1 tokens: 256 rows up to depth
   // 16 (33.8 KB), 64 rows beyond (at most 33 KB at depth 64).
   return a.depth <= 16 ? launch_walk_kernel<256>(a, stream) : launch_walk_kernel<64>(a, stream);
-}
-
-rdf2v_status launch_walk_edges(const int32_t *row_ptr, const int32_t *edges, int64_t num_edges,
-                               int32_t num_entities, int32_t *walk_edges_out, int32_t *status_dev,
-                               hipStream_t stream) {
-  if (num_edges == 0) return RDF2V_OK;
-  const int64_t blocks = (num_edges + kWalkEdgeTile - 1) / kWalkEdgeTile;
-  walk_edges_kernel<<<dim3(unsigned(blocks)), dim3(kWalkEdgeThreads), 0, stream>>>(
-      row_ptr, reinterpret_cast<const int2 *>(edges), num_edges, num_entities,
-      reinterpret_cast<v4i32 *>(walk_edges_out), status_dev);
-  RDF2V_LAUNCH_CHECK();
-  return RDF2V_OK;
 }
 
 }  // namespace rdf2v

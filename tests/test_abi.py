@@ -165,6 +165,8 @@ def test_walk_edges_argument_validation(lib):
     assert f(ctypes.byref(_csr(pkg, edges=None)), FAKE, None, None) == E_INV
     assert f(ctypes.byref(_csr(pkg, E=2**31)), FAKE, None, None) == pkg.RDF2V_ERR_TOO_LARGE
     assert f(ctypes.byref(_csr(pkg, E=0, edges=None)), None, None, None) == pkg.RDF2V_OK  # nothing to do
+    c0 = pkg._CsrStruct(0, 3, 20, FAKE, FAKE8, None)       # edges but no entity to point at
+    assert f(ctypes.byref(c0), FAKE, None, None) == pkg.RDF2V_ERR_ID_OUT_OF_RANGE
     # walks reading walk records need them 16-byte aligned
     c = pkg._CsrStruct(10, 3, 20, FAKE, FAKE8, ctypes.c_void_p((1 << 40) + 8))
     assert _walk(lib, c) == E_INV

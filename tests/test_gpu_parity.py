@@ -247,6 +247,14 @@ def test_inconsistent_csr_is_flagged_not_read():
     rd.rdf2v_random_walks(csr, to_dev([0, 2]), 8, 6, 42, status=st)
     torch.cuda.synchronize()
     assert int(st.item()) & rd.RDF2V_STATUS_BAD_CSR
+    # building walk records over an object id out of range flags it and gives that record the
+    # bounds (0, 0) of an empty row; the other records are unaffected
+    bad_edges = torch.tensor([[0, 1], [0, 7], [0, 1], [0, 3]], dtype=torch.int32, device=dev)
+    st = new_status()
+    out = rd.rdf2v_build_walk_edges(rd.Csr(good_rp, bad_edges, 4, 1), status=st).walk_edges
+    torch.cuda.synchronize()
+    assert int(st.item()) & rd.RDF2V_STATUS_ID_OUT_OF_RANGE
+    assert out.cpu().numpy().tolist() == [[0, 1, 2, 3], [0, 7, 0, 0], [0, 1, 2, 3], [0, 3, 4, 4]]
 
 
 def test_empty_and_degenerate_inputs():
