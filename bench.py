@@ -333,6 +333,90 @@ def time_vocab(rd, torch, synth, w, s, p, o, stream, ev):
             "frac_of_hbm_peak": streamed / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
 
 
+def oracle_sample(run, probe_n: int, max_n: int, seconds: float, max_units: int | None = None):
+    """Time `run(n)` -> (units, seconds) on a small probe, then on samples grown at most tenfold
+    at a time towards `seconds` of oracle time (at most max_n inputs and, judging by the last
+    run, about max_units outputs), until one takes at least half of it (the oracle's cost per
+    item grows once its outputs leave the caches). Returns (n, units, seconds) of the last run."""
+    n = max(1, min(probe_n, max_n))
+    units, dt = run(n)
+    while dt < 0.5 * seconds and n < max_n:
+        cap = max_n if not max_units or units == 0 else min(max_n, int(max_units * n / units))
+        if cap <= n:
+            break
+        n = min(cap, max(n + 1, int(n * min(10.0, 0.8 * seconds / max(dt, 1e-4)))))
+        units, dt = run(n)
+    return n, units, dt
+
+
+def cpu_oracle_legs(out, args, w, s, p, o, n_start: int, seconds: float) -> None:
+    """The oracle (untuned, one thread) beside every extra leg that ran, each on a bounded sample
+    of the same workload: the duplicate-free walks, BFS walks, skip-gram pairs and CBOW examples
+    of the oracle's own walks and CSR, and the vocabulary of a prefix of the string triples."""
+    import numpy as np
+
+    import oracle
+    import synth
+    legs = [k for k in ("unique_walks", "bfs_walks", "skipgram_pairs", "cbow_examples", "vocabulary") if k in out]
+    if not legs:
+        return
+    V, P, d, wpn = w.num_entities, w.num_predicates, w.depth, w.walks_per_node
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    starts = oracle.nonsink_starts(rp, V)
+    kind = {"triples": 0, "entities": oracle.ENTITY_WALKS, "properties": oracle.PROPERTY_WALKS}[args.tokens]
+    n_walks = n_start * wpn
+
+    def walk_rows(n):
+        tok, ln = oracle.random_walks(rp, ed, V, P, starts, wpn, d, 42, 0, n)
+        return (tok, ln) if kind == 0 else oracle.project_walks(tok, ln, d, kind)
+
+    def timed(fn):
+        t0 = time.perf_counter()
+        r = fn()
+        return r, time.perf_counter() - t0
+
+    def record(leg, unit, what, n, units, dt):
+        out[leg]["cpu_oracle"] = {"value": units / dt, "unit": unit, "cores": 1, "kind": "oracle",
+                                  "sample": f"{what} ({units:,} {unit[:-2]} in {dt:.2f} s), single thread"}
+
+    if "unique_walks" in out:
+        def run(n):
+            tok, ln = walk_rows(n)
+            _, dt = timed(lambda: oracle.unique_walks(tok, ln, wpn))
+            return n, dt
+        n, u, dt = oracle_sample(run, 20 * wpn, n_walks // wpn * wpn, seconds)
+        record("unique_walks", "walks/s", f"oracle duplicate-free walks of its walks [0, {n:,})", n, u, dt)
+    if "bfs_walks" in out:
+        bw = out["bfs_walks"]
+
+        def run(n):
+            _, dt = timed(lambda: oracle.bfs_walks(rp, ed, V, P, starts[:n], bw["depth"], bw["max_walks_per_root"]))
+            return n, dt
+        n, u, dt = oracle_sample(run, 200, n_start, seconds)
+        record("bfs_walks", "roots/s", f"oracle BFS walks from the first {n:,} start entities", n, u, dt)
+    # outputs capped at ~0.3-0.9 GB of oracle memory
+    for leg, fn, unit, max_units in (("skipgram_pairs", oracle.skipgram_pairs, "pairs/s", 40_000_000),
+                                     ("cbow_examples", oracle.cbow_examples, "examples/s", 20_000_000)):
+        if leg in out:
+            window = out[leg]["window"]
+
+            def run(n, fn=fn, window=window):
+                tok, ln = walk_rows(n)
+                r, dt = timed(lambda: fn(tok, ln, window))
+                return int(r.shape[0] if isinstance(r, np.ndarray) else r[0].shape[0]), dt
+            n, u, dt = oracle_sample(run, 20_000, n_walks, seconds, max_units)
+            record(leg, unit, f"oracle {leg.replace('_', ' ')} of its walks [0, {n:,}), window {window}",
+                   n, u, dt)
+    if "vocabulary" in out:
+        def run(n):
+            cols = synth.string_triples(s[:n], p[:n], o[:n], V, P)
+            _, dt = timed(lambda: oracle.build_vocabulary(cols[0][0], cols[0][1], cols[1][0], cols[1][1],
+                                                          cols[2][0], cols[2][1]))
+            return n, dt
+        n, u, dt = oracle_sample(run, 100_000, int(s.shape[0]), seconds)
+        record("vocabulary", "triples/s", f"oracle vocabulary of the first {n:,} string triples", n, u, dt)
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -344,6 +428,8 @@ def main() -> int:
                     help="build 16-byte walk records in the step: as rdf2v_walk_edges_recommended "
                          "advises for the graph size (auto), always, or never")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--leg-cpu-seconds", type=float, default=2.0,
+                    help="oracle time per extra leg (pairs, CBOW, BFS, duplicate-free walks, vocabulary)")
     ap.add_argument("--tokens", choices=["triples", "entities", "properties"], default="triples",
                     help="walk rows: entity/predicate triples (default), entity walks or property walks")
     ap.add_argument("--unique-walks", action="store_true",
@@ -538,6 +624,7 @@ def main() -> int:
         out["vocabulary"] = time_vocab(rd, torch, synth, w, s, p, o, stream, ev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, s, p, o, args.cpu_seconds)
+        cpu_oracle_legs(out, args, w, s, p, o, n_start, args.leg_cpu_seconds)
     print(json.dumps(out), flush=True)
     return 0
 

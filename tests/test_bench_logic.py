@@ -58,3 +58,26 @@ def test_more_than_one_gpu_is_refused():
     assert res.returncode == 2
     assert "one GPU" in res.stderr
     assert res.stdout == ""
+
+
+def test_cpu_oracle_legs_on_tiny_workload():
+    # Each extra leg that ran gets the oracle's rate on a bounded sample beside it.
+    import argparse
+
+    import bench
+    import oracle
+    import synth
+    w = synth.WORKLOADS["tiny_uniform"]
+    s, p, o = synth.triples(w)
+    rp, _ = oracle.build_csr(s, p, o, w.num_entities, w.num_predicates)
+    n_start = oracle.nonsink_starts(rp, w.num_entities).shape[0]
+    out = {"unique_walks": {}, "bfs_walks": {"depth": 2, "max_walks_per_root": 16},
+           "skipgram_pairs": {"window": 2}, "cbow_examples": {"window": 3}, "vocabulary": {}}
+    bench.cpu_oracle_legs(out, argparse.Namespace(tokens="triples"), w, s, p, o, n_start, 0.02)
+    for leg, unit in [("unique_walks", "walks/s"), ("bfs_walks", "roots/s"), ("skipgram_pairs", "pairs/s"),
+                      ("cbow_examples", "examples/s"), ("vocabulary", "triples/s")]:
+        c = out[leg]["cpu_oracle"]
+        assert c["kind"] == "oracle" and c["cores"] == 1 and c["unit"] == unit and c["value"] > 0, leg
+    out = {}
+    bench.cpu_oracle_legs(out, argparse.Namespace(tokens="triples"), w, s, p, o, n_start, 0.02)
+    assert out == {}
