@@ -394,9 +394,9 @@ def cpu_oracle_legs(out, args, w, s, p, o, n_start: int, seconds: float) -> None
             return n, dt
         n, u, dt = oracle_sample(run, 200, n_start, seconds)
         record("bfs_walks", "roots/s", f"oracle BFS walks from the first {n:,} start entities", n, u, dt)
-    # outputs capped at ~0.3-0.9 GB of oracle memory
-    for leg, fn, unit, max_units in (("skipgram_pairs", oracle.skipgram_pairs, "pairs/s", 40_000_000),
-                                     ("cbow_examples", oracle.cbow_examples, "examples/s", 20_000_000)):
+    # outputs capped at ~1.6 / 2.6 GB of oracle memory
+    for leg, fn, unit, max_units in (("skipgram_pairs", oracle.skipgram_pairs, "pairs/s", 200_000_000),
+                                     ("cbow_examples", oracle.cbow_examples, "examples/s", 60_000_000)):
         if leg in out:
             window = out[leg]["window"]
 
