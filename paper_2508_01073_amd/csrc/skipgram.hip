@@ -257,17 +257,32 @@ __global__ __launch_bounds__(kBlock) void cbow_emit_kernel(const int32_t *__rest
   const int64_t cw = 2 * int64_t(window);  // context entries per example
   int bad = 0;
   const int64_t block_first = offsets[r0];
-  int64_t L = 0;
-  if (active) L = clamped_len(len, r, width, bad);
+  // Every global read the block needs is issued before the first barrier, so
+  // none of them waits behind it: the walk's length and first example, the
+  // rows, and (thread 0) where the next block's examples begin.
+  int64_t L = 0, walk_first = 0;
+  if (active) {
+    L = clamped_len(len, r, width, bad);
+    walk_first = offsets[r];
+  }
+  __shared__ int64_t block_end;
   if (kStage) {
     const int64_t span = (r_end - r0) * width;  // <= kBlock
     if (t < span) rows[t] = tokens[r0 * width + t];
+    if (t == 0) {
+      if (r_end < n) {
+        block_end = offsets[r_end];
+      } else {
+        int b2 = 0;
+        block_end = offsets[n - 1] + clamped_len(len, n - 1, width, b2);
+      }
+    }
     __syncthreads();
   }
   bool full = false;
   if (active && i < L) {
     const int32_t *row = kStage ? rows + (t / width) * width : tokens + r * width;
-    const int64_t e = offsets[r] + i;
+    const int64_t e = walk_first + i;
     if (e >= capacity) full = true;
     if (kStage) ctr_stage[e - block_first] = row[i];
     else if (e < capacity) centers[e] = row[i];
@@ -283,13 +298,6 @@ __global__ __launch_bounds__(kBlock) void cbow_emit_kernel(const int32_t *__rest
   if (kStage) {
     __syncthreads();
     // The block's examples end where the next block's begin.
-    int64_t block_end;
-    if (r_end < n) {
-      block_end = offsets[r_end];
-    } else {
-      int b2 = 0;
-      block_end = offsets[n - 1] + clamped_len(len, n - 1, width, b2);
-    }
     const int64_t lim = max(int64_t(0), min(block_end, capacity) - block_first);  // examples that fit
     stream_run<kBlock>(ctr_stage, centers + block_first, lim);
     stream_run<kBlock>(ctx_stage, contexts + block_first * cw, lim * cw);
