@@ -278,12 +278,14 @@ __global__ __launch_bounds__(NT) void group_keep_kernel(const int32_t *__restric
   }
   const int64_t r0 = int64_t(blockIdx.x) * rows_per_block;
   const int32_t rows = int32_t(min(int64_t(rows_per_block), n - r0));
+  // The row's length is read before the barrier, alongside the rows.
+  const int32_t raw_len = t < rows ? len[r0 + t] : 0;
   stage_ints<NT>(tile, tokens + r0 * width, rows * width);
   __syncthreads();
   int bad = 0;
   int32_t L = 0, slot = 0;
   if (t < rows) {
-    L = clamp_len(len[r0 + t], width, bad);
+    L = clamp_len(raw_len, width, bad);
     const uint64_t h = row_hash(tile + t * width, L);
     hashes[t] = h;
     lens[t] = L;
@@ -341,15 +343,18 @@ __global__ __launch_bounds__(NT) void group_compact_kernel(const int32_t *__rest
   __shared__ int64_t scratch[NT / kWave];
   const int64_t r0 = int64_t(blockIdx.x) * rows_per_block;
   const int32_t rows = int32_t(min(int64_t(rows_per_block), n - r0));
-  stage_ints<NT>(tile, tokens + r0 * width, rows * width);
   const int t = threadIdx.x;
+  // Every global read is issued before the scan's barriers: the keep flag, the
+  // row's length, the block's output offset, and the rows themselves.
   const int64_t k = t < rows ? keep[r0 + t] : 0;
+  const int32_t row_len = t < rows ? len[r0 + t] : 0;
+  const int64_t out0 = partials[blockIdx.x];
+  stage_ints<NT>(tile, tokens + r0 * width, rows * width);
   int64_t tot;
   const int64_t ex = block_exclusive_scan<NT, int64_t>(k, scratch, tot);  // also orders the stage
-  const int64_t out0 = partials[blockIdx.x];
   if (k) {
     kept_rows[ex] = t;
-    len_out[out0 + ex] = len[r0 + t];
+    len_out[out0 + ex] = row_len;
   }
   __syncthreads();
   // The block's kept rows form one contiguous output range.
