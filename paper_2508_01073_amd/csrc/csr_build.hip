@@ -148,6 +148,10 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
   for (int i = threadIdx.x; i < kTileWaves * kMaxBins; i += kSortThreads) (&wave_count[0][0])[i] = 0;
   __syncthreads();
 
+  // Thread d's global start of digit d in this tile, issued with the tile's loads
+  // below so that it is not waited for on its own after the ranking barrier.
+  const int32_t digit_global = threadIdx.x < bins ? offsets[int64_t(threadIdx.x) * tiles + tile] : 0;
+
   // Wave `wave` owns tile items [wave*kWaveItems, (wave+1)*kWaveItems), visited in order.
   // All of the wave's loads are issued before any ranking, so they are in
   // flight together.
@@ -207,7 +211,7 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
         wave_count[w][d] = run;
         run += c[w];
       }
-      global_minus_local[d] = offsets[int64_t(d) * tiles + tile] - start;
+      global_minus_local[d] = digit_global - start;
     }
   }
   __syncthreads();
