@@ -1,0 +1,77 @@
+"""Seeded randomized parity: many small graphs and parameter combinations, each run through the
+HIP path (C ABI) and compared element by element with the oracle — the CSR, the start set, and
+a random window of walk ids with and without walk records, for all three token kinds, plus
+skip-gram pairs and CBOW examples of those rows. Sizes, depths (0 and the maximum included),
+walks per start, seeds (64-bit), id spaces and sink fractions are drawn per case from one master
+seed, so a failure names a case that reruns exactly."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2508_01073_amd as rd
+from gpu_helpers import assert_csr_equal, assert_rows_equal, gpu_csr, new_status, plain, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+MASTER_SEED = 20250801
+CASES = 500
+
+
+def _case(i):
+    rng = np.random.default_rng([MASTER_SEED, i])
+    V = int(rng.choice([1, 2, 3, 17, 255, 256, 257, 1000, 4096, 5000, 70_000]))
+    P = int(rng.integers(1, 60))
+    T = int(rng.choice([0, 1, 5, 100, 4095, 4096, 4097, 10_000, 50_000]))
+    depth = int(rng.choice([0, 1, 2, 3, 7, 8, 15, 16, 17, 33, 64]))
+    wpn = int(rng.integers(1, 6))
+    seed = int(rng.integers(0, 2**63)) * 2 + int(rng.integers(0, 2))
+    # subjects from a subset of the ids, so some entities are sinks
+    subj_pool = max(1, int(V * rng.uniform(0.2, 1.0)))
+    s = rng.integers(0, subj_pool, T).astype(np.int32)
+    if rng.random() < 0.5:  # skewed subjects: long rows next to short ones
+        s = (subj_pool * rng.random(T) ** 3).astype(np.int32)
+    p = rng.integers(0, P, T).astype(np.int32)
+    o = rng.integers(0, V, T).astype(np.int32)
+    return rng, V, P, s, p, o, depth, wpn, seed
+
+
+@pytest.mark.parametrize("i", range(CASES))
+def test_random_case(i):
+    rng, V, P, s, p, o, depth, wpn, seed = _case(i)
+    say(f"[fuzz] case {i}: V={V} P={P} T={s.shape[0]} depth={depth} wpn={wpn} seed={seed}")
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P, walk_records=bool(rng.random() < 0.5) and s.shape[0] > 0)
+    assert_csr_equal(csr, rp, ed)
+    starts = oracle.nonsink_starts(rp, V)
+    got = rd.rdf2v_nonsink_starts(csr)
+    assert np.array_equal(got.cpu().numpy(), starts)
+    if rng.random() < 0.3 and V > 1:  # an explicit start list with duplicates and sinks
+        starts = rng.integers(0, V, int(rng.integers(1, 50))).astype(np.int32)
+    n_walks = starts.shape[0] * wpn
+    if n_walks == 0:
+        return
+    b = int(rng.integers(0, n_walks))
+    c = int(rng.integers(1, min(n_walks - b, 20_000) + 1))
+    tr, lr = oracle.random_walks(rp, ed, V, P, starts, wpn, depth, seed, b, c)
+    sd = to_dev(starts)
+    for view, what in [(csr, "as built"), (plain(csr), "plain records")]:
+        st = new_status()
+        tok, ln = rd.rdf2v_random_walks(view, sd, wpn, depth, seed, b, c, status=st)
+        torch.cuda.synchronize()
+        rd.check_device_status(st, f"case {i}")
+        assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), tr, lr, f"case {i} walks [{b}, {b + c}) {what}")
+    for kind in (oracle.ENTITY_WALKS, oracle.PROPERTY_WALKS):
+        pt, pl = oracle.project_walks(tr, lr, depth, kind)
+        tok, ln = rd.rdf2v_random_walks_tokens(csr, sd, wpn, depth, seed, b, c, kind)
+        torch.cuda.synchronize()
+        assert_rows_equal(tok.cpu().numpy(), ln.cpu().numpy(), pt, pl, f"case {i} token kind {kind}")
+    window = int(rng.integers(1, 2 * depth + 2))
+    pairs = rd.rdf2v_skipgram_pairs(to_dev(tr), to_dev(lr), window).cpu().numpy()
+    assert np.array_equal(pairs, oracle.skipgram_pairs(tr, lr, window)), f"case {i} pairs window {window}"
+    if window <= 2 * 64:
+        cg, xg = rd.rdf2v_cbow_examples(to_dev(tr), to_dev(lr), window)
+        cr, xr = oracle.cbow_examples(tr, lr, window)
+        assert np.array_equal(cg.cpu().numpy(), cr) and np.array_equal(xg.cpu().numpy(), xr), \
+            f"case {i} CBOW window {window}"
