@@ -75,3 +75,51 @@ def test_random_case(i):
         cr, xr = oracle.cbow_examples(tr, lr, window)
         assert np.array_equal(cg.cpu().numpy(), cr) and np.array_equal(xg.cpu().numpy(), xr), \
             f"case {i} CBOW window {window}"
+
+
+GRAPH_CASES = 200
+
+
+@pytest.mark.parametrize("i", range(GRAPH_CASES))
+def test_random_bfs_and_unique_case(i):
+    # BFS walks from random roots (duplicates and sinks included) at caps that truncate and
+    # trees of every size (one-wave LDS tier up to the workspace pass), then duplicate-free walks
+    # of short walks on the same graph (many repeats) with group sizes across block boundaries.
+    rng = np.random.default_rng([MASTER_SEED, 1, i])
+    V = int(rng.choice([1, 2, 5, 64, 300, 2000, 20_000]))
+    P = int(rng.integers(1, 20))
+    T = int(V * rng.choice([0.5, 1, 2, 4, 8]))
+    subj_pool = max(1, int(V * rng.uniform(0.3, 1.0)))
+    s = (subj_pool * rng.random(T) ** (3 if rng.random() < 0.5 else 1)).astype(np.int32)
+    p = rng.integers(0, P, T).astype(np.int32)
+    o = rng.integers(0, V, T).astype(np.int32)
+    depth = int(rng.choice([0, 1, 2, 3, 4, 5]))
+    max_walks = int(rng.choice([1, 2, 7, 64, 256, 1025]))
+    roots = rng.integers(0, V, int(rng.integers(1, 200))).astype(np.int32)
+    say(f"[fuzz] graph case {i}: V={V} P={P} T={T} bfs depth={depth} max_walks={max_walks} roots={roots.size}")
+    rp, ed = oracle.build_csr(s, p, o, V, P)
+    csr = gpu_csr(s, p, o, V, P)
+    st = new_status()
+    tok, ln, cnt = rd.rdf2v_bfs_walks(csr, to_dev(roots), depth, max_walks, status=st)
+    torch.cuda.synchronize()
+    ref_t, ref_l, ref_c, trunc = oracle.bfs_walks(rp, ed, V, P, roots, depth, max_walks)
+    assert np.array_equal(cnt.cpu().numpy(), ref_c), f"case {i}: BFS walk counts"
+    valid = np.arange(max_walks)[None, :] < ref_c[:, None]
+    assert np.array_equal(tok.cpu().numpy()[valid], ref_t[valid]), f"case {i}: BFS rows"
+    assert np.array_equal(ln.cpu().numpy()[valid], ref_l[valid]), f"case {i}: BFS lengths"
+    flags = int(st.item())
+    assert bool(flags & rd.RDF2V_STATUS_CAPACITY) == (trunc > 0) and not flags & ~rd.RDF2V_STATUS_CAPACITY, \
+        f"case {i}: status {flags}"
+
+    starts = oracle.nonsink_starts(rp, V)
+    if starts.size == 0:
+        return
+    wpn = int(rng.integers(1, 9))
+    n = min(starts.size * wpn, int(rng.integers(1, 6000)))
+    wd = int(rng.integers(1, 5))
+    tr, lr = oracle.random_walks(rp, ed, V, P, starts, wpn, wd, int(rng.integers(0, 2**62)), 0, n)
+    group = int(rng.choice([1, 2, 3, wpn, 7, 64, 1025]))
+    gt, gl = rd.rdf2v_unique_walks(to_dev(tr), to_dev(lr), group)
+    rt, rl = oracle.unique_walks(tr, lr, group)
+    assert np.array_equal(gl.cpu().numpy(), rl) and np.array_equal(gt.cpu().numpy(), rt), \
+        f"case {i}: duplicate-free walks, group {group}"
