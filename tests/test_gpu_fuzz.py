@@ -123,3 +123,46 @@ def test_random_bfs_and_unique_case(i):
     rt, rl = oracle.unique_walks(tr, lr, group)
     assert np.array_equal(gl.cpu().numpy(), rl) and np.array_equal(gt.cpu().numpy(), rt), \
         f"case {i}: duplicate-free walks, group {group}"
+
+
+VOCAB_CASES = 100
+
+
+def _string_column(rng, pool, picks):
+    strs = [pool[k] for k in picks]
+    off = np.zeros(len(strs) + 1, np.int64)
+    off[1:] = np.cumsum([len(x) for x in strs])
+    chars = np.frombuffer(b"".join(strs), np.uint8) if strs and off[-1] else np.zeros(0, np.uint8)
+    return chars.copy(), off
+
+
+@pytest.mark.parametrize("i", range(VOCAB_CASES))
+def test_random_vocabulary_case(i):
+    # Byte strings from pools of near-duplicates: empty strings, NUL and 0xFF bytes, shared
+    # prefixes, lengths up to 200 (past the fast pass's 98 bytes), drawn with skew so that some
+    # strings repeat thousands of times and others once.
+    rng = np.random.default_rng([MASTER_SEED, 2, i])
+    T = int(rng.choice([0, 1, 7, 255, 256, 257, 3000, 20_000]))
+    alphabet = rng.choice([2, 4, 16, 256])
+    def pool(n):
+        out, base = [], bytes(rng.integers(0, alphabet, int(rng.integers(0, 150)), dtype=np.uint8))
+        for _ in range(n):
+            L = int(rng.choice([0, 1, 2, 5, 7, 8, 31, 97, 98, 99, 150, 200]))
+            body = bytes(rng.integers(0, alphabet, L, dtype=np.uint8))
+            out.append(base[:int(rng.integers(0, len(base) + 1))] + body if rng.random() < 0.5 else body)
+        return out
+    ent, prd = pool(int(rng.integers(1, 3000))), pool(int(rng.integers(1, 300)))
+    skew = lambda n, k: (k * rng.random(n) ** 3).astype(np.int64) if rng.random() < 0.5 else rng.integers(0, k, n)
+    cols = [_string_column(rng, ent, skew(T, len(ent))), _string_column(rng, prd, skew(T, len(prd))),
+            _string_column(rng, ent, skew(T, len(ent)))]
+    say(f"[fuzz] vocabulary case {i}: T={T} alphabet={alphabet} pools={len(ent)}/{len(prd)}")
+    ref = oracle.build_vocabulary(cols[0][0], cols[0][1], cols[1][0], cols[1][1], cols[2][0], cols[2][1])
+    dev = torch.device("cuda:0")
+    dcols = [(torch.from_numpy(c).to(dev), torch.from_numpy(o).to(dev)) for c, o in cols]
+    st = new_status()
+    s, p, o, counts = rd.rdf2v_build_vocabulary(*dcols, max(1, 2 * T), max(1, T), status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0, f"case {i}: status {int(st.item())}"
+    assert counts.cpu().numpy().tolist() == [ref[3], ref[4]], f"case {i}: distinct counts"
+    for got, want, name in zip((s, p, o), ref[:3], ("subject", "predicate", "object")):
+        assert np.array_equal(got.cpu().numpy(), want), f"case {i}: {name} ids"
