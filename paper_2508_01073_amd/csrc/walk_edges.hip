@@ -19,7 +19,7 @@ typedef int32_t v2i32 __attribute__((ext_vector_type(2)));
 // all loads, then all row-bound gathers, then all stores, so that several
 // independent memory operations per lane are in flight.
 constexpr int kWalkEdgeThreads = 256;
-constexpr int kWalkEdgeItems = 4;
+constexpr int kWalkEdgeItems = 2;
 constexpr int kWalkEdgeTile = kWalkEdgeThreads * kWalkEdgeItems;
 
 __global__ __launch_bounds__(kWalkEdgeThreads) void walk_edges_kernel(
