@@ -77,8 +77,30 @@ def traffic_from_profile(workload: str, num_walks: int):
     return pmc.get("hbm_bytes_per_launch")
 
 
+def host_cores() -> list[int]:
+    """The host cores this process may run on (its affinity set: `nproc`)."""
+    if hasattr(os, "sched_getaffinity"):
+        return sorted(os.sched_getaffinity(0))
+    return list(range(os.cpu_count() or 1))
+
+
 def cpu_baseline(w, s, p, o, target_seconds: float):
-    """The CPU oracle, untuned, single-threaded, on a bounded sample of the workload."""
+    """The CPU oracle, untuned, single-threaded and pinned to one host core, on a bounded
+    sample of the workload; then the same oracle function on all host cores."""
+    cores = host_cores()
+    if not hasattr(os, "sched_setaffinity"):
+        return _cpu_baseline(w, s, p, o, target_seconds, None, cores)
+    # Pin the calling thread (the oracle runs in it through ctypes) for the one-core leg only.
+    before = os.sched_getaffinity(0)
+    os.sched_setaffinity(0, {cores[0]})
+    try:
+        out = _cpu_baseline(w, s, p, o, target_seconds, cores[0], cores)
+    finally:
+        os.sched_setaffinity(0, before)
+    return out
+
+
+def _cpu_baseline(w, s, p, o, target_seconds: float, pinned_core, cores):
     import numpy as np
     import oracle
     V, P = w.num_entities, w.num_predicates
@@ -105,10 +127,16 @@ def cpu_baseline(w, s, p, o, target_seconds: float):
         "kind": "oracle",
         "sample": (f"oracle CSR build over all {w.num_triples:,} triples ({t_build:.2f} s, charged "
                    f"pro rata) + the first {sample:,} of {num_walks:,} walks ({t_walk:.2f} s), "
-                   f"single thread on {os.cpu_count()} visible host cores"),
+                   f"single thread pinned to host core {pinned_core} of {len(cores)}"),
+        "pinned_core": pinned_core,
+        "nproc": len(cores),
         "cpu_model": cpu_model(),
     }
-    out["all_cores"] = cpu_baseline_threads(oracle, rp, ed, V, P, starts, w, rate, target_seconds / 2)
+    # the all-core leg runs unpinned again (the caller restores the affinity set after this
+    # function returns, so restore it here for the worker threads first)
+    if pinned_core is not None:
+        os.sched_setaffinity(0, set(cores))
+    out["all_cores"] = cpu_baseline_threads(oracle, rp, ed, V, P, starts, w, rate, target_seconds / 2, cores)
     return out
 
 
@@ -132,12 +160,15 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline_threads(oracle, rp, ed, V, P, starts, w, rate_1t: float, seconds: float):
+def cpu_baseline_threads(oracle, rp, ed, V, P, starts, w, rate_1t: float, seconds: float, cores):
     """The same oracle function in N threads over disjoint walk ranges (each ctypes call runs
-    without the GIL), N = the host threads this process may use (at most 16); walks only,
-    about `seconds` of wall time."""
+    without the GIL), N = the host cores this process may run on (`nproc`), or OMP_NUM_THREADS
+    where the host sets a smaller thread budget; walks only, about `seconds` of wall time."""
     import concurrent.futures
-    n = max(1, min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()))
+    n = len(cores)
+    budget = os.environ.get("OMP_NUM_THREADS", "")
+    if budget.isdigit() and 0 < int(budget) < n:
+        n = int(budget)
     num_walks = len(starts) * w.walks_per_node
     per_thread = int(min(num_walks // n, max(1000, rate_1t * seconds)))
 
@@ -148,7 +179,7 @@ def cpu_baseline_threads(oracle, rp, ed, V, P, starts, w, rate_1t: float, second
     with concurrent.futures.ThreadPoolExecutor(max_workers=n) as pool:
         tokens = sum(pool.map(run, range(n)))
     elapsed = time.perf_counter() - t0
-    return {"value": tokens / elapsed, "unit": "tokens/s", "threads": n,
+    return {"value": tokens / elapsed, "unit": "tokens/s", "threads": n, "nproc": len(cores),
             "sample": f"walks [0, {n * per_thread:,}) in {n} disjoint ranges, {elapsed:.2f} s wall (walks only)"}
 
 
@@ -513,7 +544,7 @@ def main() -> int:
     del a, b
 
     def step(record, measure=None):
-        e0, e1, e2, e3 = ev(), ev(), ev(), ev()
+        e0, e1, e2 = ev(), ev(), ev()
         e0.record(stream)
         csr = rd.rdf2v_build_csr(subj, pred, obj, V, P, workspace=ws_build, status=status,
                                  row_ptr=row_ptr, edges=edges, stream=stream)
@@ -526,16 +557,20 @@ def main() -> int:
         e2.record(stream)
         n_walks = n_start * wpn
         launches = 0
+        batch_events = []  # one event after each walk launch (batches of the 500M-triple share)
         for b0 in range(0, n_walks, batch_cap):
             c = min(batch_cap, n_walks - b0)
             rd.rdf2v_random_walks_tokens(csr, st[:n_start], wpn, d, 42, b0, c, kind, tokens=tokens[:c],
                                          lens=lens[:c], status=status, stream=stream)
             launches += 1
+            eb = ev()
+            eb.record(stream)
+            batch_events.append(eb)
             if measure is not None:
                 starts_read = (b0 + c + wpn - 1) // wpn - b0 // wpn
                 measure.append(useful_bytes(lens[:c], d, starts_read, kind))
-        e3.record(stream)
-        record.append((e0, e1, e2, e3, n_start, launches))
+        e3 = batch_events[-1] if batch_events else e2
+        record.append((e0, e1, e2, e3, n_start, launches, batch_events))
 
     warm = []
     for _ in range(max(args.warmup, 1) - 1):
@@ -561,9 +596,17 @@ def main() -> int:
 
     elapsed = t1 - t0
     ms_step = 1e3 * elapsed / args.steps
-    build_ms = float(np.mean([r[0].elapsed_time(r[1]) for r in rec]))
-    starts_ms = float(np.mean([r[1].elapsed_time(r[2]) for r in rec]))
-    walk_ms = float(np.mean([r[2].elapsed_time(r[3]) for r in rec]))  # all walk launches of a step
+    # HIP-event times of every timed step: the CSR build (+ walk records), the start set, all
+    # walk launches of the step, and the whole step on the GPU; means and medians of these
+    build_t = [r[0].elapsed_time(r[1]) for r in rec]
+    starts_t = [r[1].elapsed_time(r[2]) for r in rec]
+    walk_t = [r[2].elapsed_time(r[3]) for r in rec]
+    step_t = [r[0].elapsed_time(r[3]) for r in rec]
+    build_ms, starts_ms, walk_ms = float(np.mean(build_t)), float(np.mean(starts_t)), float(np.mean(walk_t))
+    walk_med = float(np.median(walk_t))
+    # per-batch walk times (one entry per launch of a step), median over the timed steps
+    batch_ms = [float(np.median([(r[2] if i == 0 else r[6][i - 1]).elapsed_time(r[6][i]) for r in rec]))
+                for i in range(launches)]
     achieved = ub / (walk_ms * 1e-3) / 1e9
     traffic = traffic_from_profile(w.name, n_walks) if launches == 1 else None
 
@@ -594,14 +637,28 @@ def main() -> int:
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": traffic,
+            "traffic_source": (None if traffic is None else
+                               "profiles/walk_kernel_pmc.json: rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE "
+                               "of this bench on the same workload, each scaled by its reading for a 1 GiB "
+                               "device copy; a committed profile matched by a hash of the walk kernel's "
+                               "sources, not read in this run"),
+            "achieved_median": ub / (walk_med * 1e-3) / 1e9,
+            "frac_median": ub / (walk_med * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "useful_bytes_per_launch": ub if launches == 1 else None,
             "useful_bytes_per_step": ub,
             "launches_per_step": launches,
         },
         "copy_reference_GBps": copy_gbs,
         "walk_kernel_ms": walk_ms,
+        "walk_kernel_ms_median": walk_med,
+        "walk_kernel_ms_min_max": [float(np.min(walk_t)), float(np.max(walk_t))],
+        "walk_batch_ms_median": batch_ms if launches > 1 else None,
         "build_csr_ms": build_ms,
+        "build_csr_ms_median": float(np.median(build_t)),
         "nonsink_starts_ms": starts_ms,
+        "nonsink_starts_ms_median": float(np.median(starts_t)),
+        "step_gpu_ms_median": float(np.median(step_t)),
+        "step_gpu_ms_min_max": [float(np.min(step_t)), float(np.max(step_t))],
         "valid_tokens_per_step": ntok,
         "hops_per_step": hops,
         "walk_kernel_tokens_per_s": ntok / (walk_ms * 1e-3),

@@ -15,6 +15,7 @@ with -1 (Sec. 3.1), all walks of all start entities launched together
 
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 from dataclasses import dataclass
@@ -181,10 +182,25 @@ def _ptr(t: torch.Tensor | None):
     return None if t is None or t.numel() == 0 else ctypes.c_void_p(t.data_ptr())
 
 
-def _stream(device: torch.device, stream) -> ctypes.c_void_p:
+@contextlib.contextmanager
+def _on_stream(device: torch.device, stream):
+    """Makes the caller's stream current for the whole call and yields its handle.
+
+    Everything the binding does for a call then happens on that stream: tensors it allocates
+    (outputs, workspaces) belong to it in torch's caching allocator, so a workspace freed when
+    the call returns is reused only by work ordered after the call's kernels, and a count read
+    back with ``.item()`` waits for those kernels. ``stream`` is None (the device's current
+    stream), a ``torch.cuda.Stream`` or a raw hipStream_t handle (int)."""
     if stream is None:
-        stream = torch.cuda.current_stream(device)
-    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+        s = torch.cuda.current_stream(device)
+    elif isinstance(stream, torch.cuda.Stream):
+        s = stream
+    else:
+        s = torch.cuda.ExternalStream(int(stream), device=device)
+    if s.device != device:
+        raise TypeError(f"stream is on {s.device}, the call's tensors on {device}")
+    with torch.cuda.stream(s):
+        yield ctypes.c_void_p(s.cuda_stream)
 
 
 @dataclass
@@ -225,23 +241,24 @@ def rdf2v_build_csr(subj: torch.Tensor, pred: torch.Tensor, obj: torch.Tensor, n
     if pred.shape[0] != t or obj.shape[0] != t:
         raise ValueError("subj, pred and obj differ in length")
     dev = subj.device
-    _same_device(dev, pred=pred, obj=obj)
-    if row_ptr is None:
-        row_ptr = torch.empty(num_entities + 1, dtype=torch.int32, device=dev)
-    if edges is None:
-        edges = torch.empty((t, 2), dtype=torch.int32, device=dev)
-    _out(row_ptr, "row_ptr", torch.int32, num_entities + 1, dev)
-    _out(edges, "edges", torch.int32, 2 * t, dev)
-    _status(status, dev)
-    need = rdf2v_build_csr_workspace_size(t, num_entities)
-    if workspace is None and need > 0:
-        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
-    ws_bytes = _ws_bytes(workspace)
-    st = _native().rdf2v_build_csr(_ptr(subj), _ptr(pred), _ptr(obj), t, num_entities, num_predicates,
-                              _ptr(row_ptr), _ptr(edges), _ptr(workspace), ws_bytes, _ptr(status),
-                              _stream(dev, stream))
-    _check(st, "rdf2v_build_csr")
-    return Csr(row_ptr, edges, num_entities, num_predicates)
+    with _on_stream(dev, stream) as h:
+        _same_device(dev, pred=pred, obj=obj)
+        if row_ptr is None:
+            row_ptr = torch.empty(num_entities + 1, dtype=torch.int32, device=dev)
+        if edges is None:
+            edges = torch.empty((t, 2), dtype=torch.int32, device=dev)
+        _out(row_ptr, "row_ptr", torch.int32, num_entities + 1, dev)
+        _out(edges, "edges", torch.int32, 2 * t, dev)
+        _status(status, dev)
+        need = rdf2v_build_csr_workspace_size(t, num_entities)
+        if workspace is None and need > 0:
+            workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+        ws_bytes = _ws_bytes(workspace)
+        st = _native().rdf2v_build_csr(_ptr(subj), _ptr(pred), _ptr(obj), t, num_entities, num_predicates,
+                                  _ptr(row_ptr), _ptr(edges), _ptr(workspace), ws_bytes, _ptr(status),
+                                  h)
+        _check(st, "rdf2v_build_csr")
+        return Csr(row_ptr, edges, num_entities, num_predicates)
 
 
 def rdf2v_build_walk_edges(csr: Csr, *, out: torch.Tensor | None = None,
@@ -249,15 +266,16 @@ def rdf2v_build_walk_edges(csr: Csr, *, out: torch.Tensor | None = None,
     """Returns the Csr with walk_edges [num_edges, 4] = (predicate, object, row lo, row hi)
     of the object, so the walks read one 16-byte record per hop."""
     dev = csr.row_ptr.device
-    if out is None:
-        out = torch.empty((csr.num_edges, 4), dtype=torch.int32, device=dev)
-    _same_device(dev, edges=csr.edges)
-    _out(out, "out", torch.int32, 4 * csr.num_edges, dev)
-    _status(status, dev)
-    c = csr._c()
-    st = _native().rdf2v_build_walk_edges(ctypes.byref(c), _ptr(out), _ptr(status), _stream(dev, stream))
-    _check(st, "rdf2v_build_walk_edges")
-    return Csr(csr.row_ptr, csr.edges, csr.num_entities, csr.num_predicates, out)
+    with _on_stream(dev, stream) as h:
+        if out is None:
+            out = torch.empty((csr.num_edges, 4), dtype=torch.int32, device=dev)
+        _same_device(dev, edges=csr.edges)
+        _out(out, "out", torch.int32, 4 * csr.num_edges, dev)
+        _status(status, dev)
+        c = csr._c()
+        st = _native().rdf2v_build_walk_edges(ctypes.byref(c), _ptr(out), _ptr(status), h)
+        _check(st, "rdf2v_build_walk_edges")
+        return Csr(csr.row_ptr, csr.edges, csr.num_entities, csr.num_predicates, out)
 
 
 def rdf2v_walk_edges_recommended(num_entities: int, num_edges: int) -> bool:
@@ -276,22 +294,23 @@ def rdf2v_nonsink_starts(csr: Csr, *, workspace: torch.Tensor | None = None, str
     """Entities with out-degree >= 1, ascending. With sync=True returns the int32 tensor of
     start ids (one device-to-host read of the count); else (starts, count_device_int64)."""
     dev = csr.row_ptr.device
-    if starts is None:
-        starts = torch.empty(max(csr.num_entities, 1), dtype=torch.int32, device=dev)
-    if count is None:
-        count = torch.empty(1, dtype=torch.int64, device=dev)
-    if workspace is None:
-        workspace = torch.empty(rdf2v_nonsink_starts_workspace_size(csr.num_entities),
-                                dtype=torch.uint8, device=dev)
-    _out(starts, "starts", torch.int32, csr.num_entities, dev)
-    _out(count, "count", torch.int64, 1, dev)
-    c = csr._c()
-    st = _native().rdf2v_nonsink_starts(ctypes.byref(c), _ptr(starts), _ptr(count), _ptr(workspace),
-                                   _ws_bytes(workspace), _stream(dev, stream))
-    _check(st, "rdf2v_nonsink_starts")
-    if not sync:
-        return starts, count
-    return starts[: int(count.item())]
+    with _on_stream(dev, stream) as h:
+        if starts is None:
+            starts = torch.empty(max(csr.num_entities, 1), dtype=torch.int32, device=dev)
+        if count is None:
+            count = torch.empty(1, dtype=torch.int64, device=dev)
+        if workspace is None:
+            workspace = torch.empty(rdf2v_nonsink_starts_workspace_size(csr.num_entities),
+                                    dtype=torch.uint8, device=dev)
+        _out(starts, "starts", torch.int32, csr.num_entities, dev)
+        _out(count, "count", torch.int64, 1, dev)
+        c = csr._c()
+        st = _native().rdf2v_nonsink_starts(ctypes.byref(c), _ptr(starts), _ptr(count), _ptr(workspace),
+                                       _ws_bytes(workspace), h)
+        _check(st, "rdf2v_nonsink_starts")
+        if not sync:
+            return starts, count
+        return starts[: int(count.item())]
 
 
 def rdf2v_random_walks(csr: Csr, start_nodes: torch.Tensor, walks_per_node: int, depth: int,
@@ -319,26 +338,27 @@ def _walks(csr, start_nodes, walks_per_node, depth, seed, walk_begin, walk_count
            tokens, lens, status, stream, where):
     _dev_i32(start_nodes, "start_nodes")
     dev = start_nodes.device
-    num_walks = start_nodes.shape[0] * walks_per_node
-    if walk_count is None:
-        walk_count = num_walks - walk_begin
-    width = 2 * depth + 1 if token_kind == RDF2V_TOKENS_TRIPLES else depth + 1
-    if tokens is None:
-        tokens = torch.empty((max(walk_count, 0), max(width, 1)), dtype=torch.int32, device=dev)
-    if lens is None:
-        lens = torch.empty(max(walk_count, 0), dtype=torch.int32, device=dev)
-    rows = max(walk_count, 0)
-    _out(tokens, "tokens", torch.int32, rows * width, dev)
-    _out(lens, "lens", torch.int32, rows, dev)
-    _status(status, dev)
-    _same_device(dev, row_ptr=csr.row_ptr, edges=csr.edges, walk_edges=csr.walk_edges)
-    c = csr._c()
-    st = _native().rdf2v_random_walks_tokens(ctypes.byref(c), _ptr(start_nodes), start_nodes.shape[0],
-                                             walks_per_node, depth, ctypes.c_uint64(seed & (2**64 - 1)),
-                                             walk_begin, walk_count, token_kind, _ptr(tokens), _ptr(lens),
-                                             _ptr(status), _stream(dev, stream))
-    _check(st, where)
-    return tokens, lens
+    with _on_stream(dev, stream) as h:
+        num_walks = start_nodes.shape[0] * walks_per_node
+        if walk_count is None:
+            walk_count = num_walks - walk_begin
+        width = 2 * depth + 1 if token_kind == RDF2V_TOKENS_TRIPLES else depth + 1
+        if tokens is None:
+            tokens = torch.empty((max(walk_count, 0), max(width, 1)), dtype=torch.int32, device=dev)
+        if lens is None:
+            lens = torch.empty(max(walk_count, 0), dtype=torch.int32, device=dev)
+        rows = max(walk_count, 0)
+        _out(tokens, "tokens", torch.int32, rows * width, dev)
+        _out(lens, "lens", torch.int32, rows, dev)
+        _status(status, dev)
+        _same_device(dev, row_ptr=csr.row_ptr, edges=csr.edges, walk_edges=csr.walk_edges)
+        c = csr._c()
+        st = _native().rdf2v_random_walks_tokens(ctypes.byref(c), _ptr(start_nodes), start_nodes.shape[0],
+                                                 walks_per_node, depth, ctypes.c_uint64(seed & (2**64 - 1)),
+                                                 walk_begin, walk_count, token_kind, _ptr(tokens), _ptr(lens),
+                                                 _ptr(status), h)
+        _check(st, where)
+        return tokens, lens
 
 
 def rdf2v_unique_walks_workspace_size(num_walks: int) -> int:
@@ -354,29 +374,30 @@ def rdf2v_unique_walks(tokens: torch.Tensor, lens: torch.Tensor, group_size: int
     device-to-host read of the count); else (tokens_out, lens_out, count_device_int64)."""
     _dev_i32(tokens, "tokens"); _dev_i32(lens, "lens")
     dev = tokens.device
-    n = int(lens.shape[0])
-    width = int(tokens.shape[1]) if tokens.dim() == 2 else 1
-    if tokens_out is None:
-        tokens_out = torch.empty((n, width), dtype=torch.int32, device=dev)
-    if lens_out is None:
-        lens_out = torch.empty(n, dtype=torch.int32, device=dev)
-    if count is None:
-        count = torch.empty(1, dtype=torch.int64, device=dev)
-    if workspace is None:
-        workspace = torch.empty(max(rdf2v_unique_walks_workspace_size(n), 1), dtype=torch.uint8, device=dev)
-    _same_device(dev, lens=lens)
-    _out(tokens_out, "tokens_out", torch.int32, n * width, dev)
-    _out(lens_out, "lens_out", torch.int32, n, dev)
-    _out(count, "count", torch.int64, 1, dev)
-    _status(status, dev)
-    st = _native().rdf2v_unique_walks(_ptr(tokens), _ptr(lens), n, group_size, width, _ptr(tokens_out),
-                                      _ptr(lens_out), _ptr(count), _ptr(workspace), _ws_bytes(workspace),
-                                      _ptr(status), _stream(dev, stream))
-    _check(st, "rdf2v_unique_walks")
-    if not sync:
-        return tokens_out, lens_out, count
-    k = int(count.item())
-    return tokens_out[:k], lens_out[:k]
+    with _on_stream(dev, stream) as h:
+        n = int(lens.shape[0])
+        width = int(tokens.shape[1]) if tokens.dim() == 2 else 1
+        if tokens_out is None:
+            tokens_out = torch.empty((n, width), dtype=torch.int32, device=dev)
+        if lens_out is None:
+            lens_out = torch.empty(n, dtype=torch.int32, device=dev)
+        if count is None:
+            count = torch.empty(1, dtype=torch.int64, device=dev)
+        if workspace is None:
+            workspace = torch.empty(max(rdf2v_unique_walks_workspace_size(n), 1), dtype=torch.uint8, device=dev)
+        _same_device(dev, lens=lens)
+        _out(tokens_out, "tokens_out", torch.int32, n * width, dev)
+        _out(lens_out, "lens_out", torch.int32, n, dev)
+        _out(count, "count", torch.int64, 1, dev)
+        _status(status, dev)
+        st = _native().rdf2v_unique_walks(_ptr(tokens), _ptr(lens), n, group_size, width, _ptr(tokens_out),
+                                          _ptr(lens_out), _ptr(count), _ptr(workspace), _ws_bytes(workspace),
+                                          _ptr(status), h)
+        _check(st, "rdf2v_unique_walks")
+        if not sync:
+            return tokens_out, lens_out, count
+        k = int(count.item())
+        return tokens_out[:k], lens_out[:k]
 
 
 def rdf2v_bfs_walks_workspace_size(num_entities: int, num_roots: int) -> int:
@@ -391,28 +412,29 @@ def rdf2v_bfs_walks(csr: Csr, roots: torch.Tensor, depth: int, max_walks: int, *
     rows past counts[r] are left as allocated (filled with -1 / 0 when allocated here)."""
     _dev_i32(roots, "roots")
     dev = roots.device
-    R = int(roots.shape[0])
-    width = 2 * depth + 1
-    if tokens is None:
-        tokens = torch.full((R, max_walks, width), -1, dtype=torch.int32, device=dev)
-    if lens is None:
-        lens = torch.zeros((R, max_walks), dtype=torch.int32, device=dev)
-    if counts is None:
-        counts = torch.empty(R, dtype=torch.int32, device=dev)
-    if workspace is None:
-        workspace = torch.empty(max(rdf2v_bfs_walks_workspace_size(csr.num_entities, R), 1),
-                                dtype=torch.uint8, device=dev)
-    _same_device(dev, row_ptr=csr.row_ptr, edges=csr.edges)
-    _out(tokens, "tokens", torch.int32, R * max(max_walks, 0) * width, dev)
-    _out(lens, "lens", torch.int32, R * max(max_walks, 0), dev)
-    _out(counts, "counts", torch.int32, R, dev)
-    _status(status, dev)
-    c = csr._c()
-    st = _native().rdf2v_bfs_walks(ctypes.byref(c), _ptr(roots), R, depth, max_walks, _ptr(tokens), _ptr(lens),
-                                   _ptr(counts), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
-                                   _stream(dev, stream))
-    _check(st, "rdf2v_bfs_walks")
-    return tokens, lens, counts
+    with _on_stream(dev, stream) as h:
+        R = int(roots.shape[0])
+        width = 2 * depth + 1
+        if tokens is None:
+            tokens = torch.full((R, max_walks, width), -1, dtype=torch.int32, device=dev)
+        if lens is None:
+            lens = torch.zeros((R, max_walks), dtype=torch.int32, device=dev)
+        if counts is None:
+            counts = torch.empty(R, dtype=torch.int32, device=dev)
+        if workspace is None:
+            workspace = torch.empty(max(rdf2v_bfs_walks_workspace_size(csr.num_entities, R), 1),
+                                    dtype=torch.uint8, device=dev)
+        _same_device(dev, row_ptr=csr.row_ptr, edges=csr.edges)
+        _out(tokens, "tokens", torch.int32, R * max(max_walks, 0) * width, dev)
+        _out(lens, "lens", torch.int32, R * max(max_walks, 0), dev)
+        _out(counts, "counts", torch.int32, R, dev)
+        _status(status, dev)
+        c = csr._c()
+        st = _native().rdf2v_bfs_walks(ctypes.byref(c), _ptr(roots), R, depth, max_walks, _ptr(tokens), _ptr(lens),
+                                       _ptr(counts), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
+                                       h)
+        _check(st, "rdf2v_bfs_walks")
+        return tokens, lens, counts
 
 
 def rdf2v_skipgram_pairs_workspace_size(num_walks: int) -> int:
@@ -430,33 +452,34 @@ def rdf2v_skipgram_pairs(tokens: torch.Tensor, lens: torch.Tensor, window: int, 
     the count, and a second call fills a tensor of exactly that size, which is returned."""
     _dev_i32(tokens, "tokens"); _dev_i32(lens, "lens")
     dev = tokens.device
-    w = int(lens.shape[0])
-    width = int(tokens.shape[1]) if tokens.dim() == 2 else 1
-    if workspace is None:
-        workspace = torch.empty(max(rdf2v_skipgram_pairs_workspace_size(w), 1), dtype=torch.uint8, device=dev)
-    if count is None:
-        count = torch.empty(1, dtype=torch.int64, device=dev)
-    _same_device(dev, lens=lens)
-    _out(count, "count", torch.int64, 1, dev)
-    _status(status, dev)
+    with _on_stream(dev, stream) as h:
+        w = int(lens.shape[0])
+        width = int(tokens.shape[1]) if tokens.dim() == 2 else 1
+        if workspace is None:
+            workspace = torch.empty(max(rdf2v_skipgram_pairs_workspace_size(w), 1), dtype=torch.uint8, device=dev)
+        if count is None:
+            count = torch.empty(1, dtype=torch.int64, device=dev)
+        _same_device(dev, lens=lens)
+        _out(count, "count", torch.int64, 1, dev)
+        _status(status, dev)
 
-    def call(out, cap):
-        st = _native().rdf2v_skipgram_pairs(_ptr(tokens), _ptr(lens), w, width, window, _ptr(out), cap,
-                                          _ptr(count), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
-                                          _stream(dev, stream))
-        _check(st, "rdf2v_skipgram_pairs")
+        def call(out, cap):
+            st = _native().rdf2v_skipgram_pairs(_ptr(tokens), _ptr(lens), w, width, window, _ptr(out), cap,
+                                              _ptr(count), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
+                                              h)
+            _check(st, "rdf2v_skipgram_pairs")
 
-    if pairs is not None:
-        if pairs.dim() != 2 or pairs.shape[1] != 2:
-            raise ValueError("pairs must have shape [capacity, 2]")
-        _out(pairs, "pairs", torch.int32, 0, dev)
-        call(pairs, int(pairs.shape[0]))
-        return pairs, count
-    call(None, 0)
-    n = int(count.item())
-    out = torch.empty((n, 2), dtype=torch.int32, device=dev)
-    call(out, n)
-    return out
+        if pairs is not None:
+            if pairs.dim() != 2 or pairs.shape[1] != 2:
+                raise ValueError("pairs must have shape [capacity, 2]")
+            _out(pairs, "pairs", torch.int32, 0, dev)
+            call(pairs, int(pairs.shape[0]))
+            return pairs, count
+        call(None, 0)
+        n = int(count.item())
+        out = torch.empty((n, 2), dtype=torch.int32, device=dev)
+        call(out, n)
+        return out
 
 
 def rdf2v_cbow_examples_workspace_size(num_walks: int) -> int:
@@ -476,36 +499,37 @@ def rdf2v_cbow_examples(tokens: torch.Tensor, lens: torch.Tensor, window: int, *
     call fills tensors of exactly that size, which are returned as (centers, contexts)."""
     _dev_i32(tokens, "tokens"); _dev_i32(lens, "lens")
     dev = tokens.device
-    w = int(lens.shape[0])
-    width = int(tokens.shape[1]) if tokens.dim() == 2 else 1
-    if workspace is None:
-        workspace = torch.empty(max(rdf2v_cbow_examples_workspace_size(w), 1), dtype=torch.uint8, device=dev)
-    if count is None:
-        count = torch.empty(1, dtype=torch.int64, device=dev)
-    _same_device(dev, lens=lens)
-    _out(count, "count", torch.int64, 1, dev)
-    _status(status, dev)
+    with _on_stream(dev, stream) as h:
+        w = int(lens.shape[0])
+        width = int(tokens.shape[1]) if tokens.dim() == 2 else 1
+        if workspace is None:
+            workspace = torch.empty(max(rdf2v_cbow_examples_workspace_size(w), 1), dtype=torch.uint8, device=dev)
+        if count is None:
+            count = torch.empty(1, dtype=torch.int64, device=dev)
+        _same_device(dev, lens=lens)
+        _out(count, "count", torch.int64, 1, dev)
+        _status(status, dev)
 
-    def call(c, x, cap):
-        st = _native().rdf2v_cbow_examples(_ptr(tokens), _ptr(lens), w, width, window, _ptr(c), _ptr(x), cap,
-                                           _ptr(count), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
-                                           _stream(dev, stream))
-        _check(st, "rdf2v_cbow_examples")
+        def call(c, x, cap):
+            st = _native().rdf2v_cbow_examples(_ptr(tokens), _ptr(lens), w, width, window, _ptr(c), _ptr(x), cap,
+                                               _ptr(count), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
+                                               h)
+            _check(st, "rdf2v_cbow_examples")
 
-    if (centers is None) != (contexts is None):
-        raise ValueError("give both centers and contexts, or neither")
-    if centers is not None:
-        cap = int(centers.numel())
-        _out(centers, "centers", torch.int32, 0, dev)
-        _out(contexts, "contexts", torch.int32, cap * 2 * max(window, 0), dev)
-        call(centers, contexts, cap)
-        return centers, contexts, count
-    call(None, None, 0)
-    n = int(count.item())
-    c = torch.empty(n, dtype=torch.int32, device=dev)
-    x = torch.empty((n, 2 * window), dtype=torch.int32, device=dev)
-    call(c, x, n)
-    return c, x
+        if (centers is None) != (contexts is None):
+            raise ValueError("give both centers and contexts, or neither")
+        if centers is not None:
+            cap = int(centers.numel())
+            _out(centers, "centers", torch.int32, 0, dev)
+            _out(contexts, "contexts", torch.int32, cap * 2 * max(window, 0), dev)
+            call(centers, contexts, cap)
+            return centers, contexts, count
+        call(None, None, 0)
+        n = int(count.item())
+        c = torch.empty(n, dtype=torch.int32, device=dev)
+        x = torch.empty((n, 2 * window), dtype=torch.int32, device=dev)
+        call(c, x, n)
+        return c, x
 
 
 def rdf2v_build_vocabulary_workspace_size(num_triples: int, max_entities: int, max_predicates: int) -> int:
@@ -535,24 +559,25 @@ def rdf2v_build_vocabulary(subj, pred, obj, max_entities: int, max_predicates: i
     (distinct entities, distinct predicates); no host synchronisation."""
     offsets = subj[1]
     dev = offsets.device
-    n = int(offsets.shape[0]) - 1
-    args = (_string_column(subj, "subj", n) + _string_column(pred, "pred", n) + _string_column(obj, "obj", n))
-    if ids is None:
-        ids = tuple(torch.empty(n, dtype=torch.int32, device=dev) for _ in range(3))
-    for i, name in zip(ids, ("subj_ids", "pred_ids", "obj_ids")):
-        _out(i, name, torch.int32, n, dev)
-    if counts is None:
-        counts = torch.empty(2, dtype=torch.int64, device=dev)
-    _out(counts, "counts", torch.int64, 2, dev)
-    _status(status, dev)
-    if workspace is None:
-        need = rdf2v_build_vocabulary_workspace_size(n, max_entities, max_predicates)
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    st = _native().rdf2v_build_vocabulary(*args, n, max_entities, max_predicates, *[_ptr(i) for i in ids],
-                                          _ptr(counts), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
-                                          _stream(dev, stream))
-    _check(st, "rdf2v_build_vocabulary")
-    return ids[0], ids[1], ids[2], counts
+    with _on_stream(dev, stream) as h:
+        n = int(offsets.shape[0]) - 1
+        args = (_string_column(subj, "subj", n) + _string_column(pred, "pred", n) + _string_column(obj, "obj", n))
+        if ids is None:
+            ids = tuple(torch.empty(n, dtype=torch.int32, device=dev) for _ in range(3))
+        for i, name in zip(ids, ("subj_ids", "pred_ids", "obj_ids")):
+            _out(i, name, torch.int32, n, dev)
+        if counts is None:
+            counts = torch.empty(2, dtype=torch.int64, device=dev)
+        _out(counts, "counts", torch.int64, 2, dev)
+        _status(status, dev)
+        if workspace is None:
+            need = rdf2v_build_vocabulary_workspace_size(n, max_entities, max_predicates)
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        st = _native().rdf2v_build_vocabulary(*args, n, max_entities, max_predicates, *[_ptr(i) for i in ids],
+                                              _ptr(counts), _ptr(workspace), _ws_bytes(workspace), _ptr(status),
+                                              h)
+        _check(st, "rdf2v_build_vocabulary")
+        return ids[0], ids[1], ids[2], counts
 
 
 def check_device_status(status: torch.Tensor, where: str = "device") -> None:

@@ -81,3 +81,21 @@ def test_cpu_oracle_legs_on_tiny_workload():
     out = {}
     bench.cpu_oracle_legs(out, argparse.Namespace(tokens="triples"), w, s, p, o, n_start, 0.02)
     assert out == {}
+
+
+def test_cpu_baseline_pins_one_core_and_restores_affinity():
+    # The one-thread oracle leg runs pinned to one host core, the all-core leg on every core the
+    # process may use (or the host's OMP_NUM_THREADS budget when smaller), and the process gets
+    # its affinity set back afterwards.
+    import synth
+    w = synth.WORKLOADS["tiny_uniform"]
+    s, p, o = synth.triples(w)
+    before = os.sched_getaffinity(0)
+    out = bench.cpu_baseline(w, s, p, o, 0.05)
+    assert os.sched_getaffinity(0) == before
+    assert out["cores"] == 1 and out["kind"] == "oracle" and out["value"] > 0
+    assert out["pinned_core"] in before and out["nproc"] == len(before)
+    assert f"pinned to host core {out['pinned_core']}" in out["sample"]
+    budget = os.environ.get("OMP_NUM_THREADS", "")
+    expect = min(len(before), int(budget)) if budget.isdigit() and int(budget) > 0 else len(before)
+    assert out["all_cores"]["threads"] == expect and out["all_cores"]["nproc"] == len(before)

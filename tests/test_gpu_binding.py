@@ -100,3 +100,30 @@ def test_vocabulary_outputs():
     with pytest.raises(ValueError):
         rd.rdf2v_build_vocabulary(*dcols, w.num_entities, w.num_predicates,
                                   counts=torch.empty(1, dtype=torch.int64, device=dev))
+
+
+def test_calls_on_a_side_stream(graph):
+    """A call given a stream that is not the current one allocates, launches and reads its count
+    on that stream: a start set or pair count read right after long work was queued on the side
+    stream waits for that work, and the workspace is not handed to other work while the side
+    stream still uses it."""
+    V, P, (s, p, o), csr, starts = graph
+    say("[binding] calls on a non-current stream behind queued work")
+    torch.cuda.synchronize()
+    ref_starts = starts.clone()
+    tok_ref, ln_ref = rd.rdf2v_random_walks(csr, starts, 4000, 8, 7)
+    pairs_ref = rd.rdf2v_skipgram_pairs(tok_ref, ln_ref, 5)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream(device=device())
+    side.wait_stream(torch.cuda.current_stream())
+    for handle in (side, side.cuda_stream):                       # a torch stream, then a raw handle
+        # about 2M walks of 8 hops queued on the side stream, then calls whose results the host
+        # reads at once
+        tok, ln = rd.rdf2v_random_walks(csr, starts, 4000, 8, 7, stream=handle)
+        got = rd.rdf2v_nonsink_starts(csr, stream=handle)
+        assert torch.equal(got, ref_starts)
+        pairs = rd.rdf2v_skipgram_pairs(tok, ln, 5, stream=handle)
+        assert pairs.shape == pairs_ref.shape
+        side.synchronize()
+        assert torch.equal(pairs, pairs_ref)
+        assert torch.equal(tok, tok_ref) and torch.equal(ln, ln_ref)
