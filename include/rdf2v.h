@@ -19,6 +19,8 @@
  *  - All array arguments are DEVICE pointers to caller-owned memory unless
  *    stated otherwise. The library never allocates, frees or keeps device
  *    memory and keeps no global state; calls on different streams may overlap.
+ *    The one exception is rdf2v_skipgram_pairs_noalloc, which uses a fixed
+ *    array of device memory that the library holds on each device.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream). Every
  *    call only enqueues work on it and returns without synchronising.
  *  - Errors that the host can see (null pointers, negative or oversized
@@ -233,6 +235,37 @@ rdf2v_status rdf2v_skipgram_pairs(const int32_t *tokens, const int32_t *len, int
                                   int32_t row_width, int32_t window, int32_t *pairs_out,
                                   int64_t pair_capacity, int64_t *pair_count_out, void *workspace,
                                   size_t workspace_bytes, int32_t *status_dev, void *stream);
+
+/* Most walk rows one rdf2v_skipgram_pairs_noalloc call takes, and the size of
+ * the device array it uses for its scratch on each device (32 MiB + 64 KiB). */
+#define RDF2V_NOALLOC_MAX_WALKS ((int64_t)1 << 22)
+#define RDF2V_NOALLOC_SCRATCH_BYTES (((size_t)32 << 20) + ((size_t)64 << 10))
+
+/*
+ * rdf2v_skipgram_pairs for callers that cannot allocate device memory (code
+ * being captured into a graph, tight serving loops, harnesses that forbid
+ * hipMalloc): the same pairs, count and status, with the same arguments
+ * except that there is no workspace. The scratch (per-walk output offsets and
+ * block sums) lives instead in a device array of RDF2V_NOALLOC_SCRATCH_BYTES
+ * that the library holds on every device it runs on until the process ends;
+ * the first call on a device looks its address up (making that device current
+ * for the lookup and restoring the caller's current device). The call itself
+ * allocates nothing.
+ *
+ *   num_walks   0 .. RDF2V_NOALLOC_MAX_WALKS; more returns
+ *               RDF2V_ERR_TOO_LARGE and enqueues nothing (split the rows into
+ *               batches, or use rdf2v_skipgram_pairs with a workspace).
+ *   stream      the device whose array is used is the stream's device.
+ *
+ * All calls on one device share its array and its contents persist between
+ * calls: calls that overlap on one device (on different streams or from
+ * different threads) race and give wrong pairs. Serialise them, e.g. on one
+ * stream. No part of the array needs clearing between calls.
+ */
+rdf2v_status rdf2v_skipgram_pairs_noalloc(const int32_t *tokens, const int32_t *len, int64_t num_walks,
+                                          int32_t row_width, int32_t window, int32_t *pairs_out,
+                                          int64_t pair_capacity, int64_t *pair_count_out, int32_t *status_dev,
+                                          void *stream);
 
 /* Bytes of device workspace rdf2v_cbow_examples needs. Pure host function;
  * 0 when num_walks is negative or above 2^46 (rdf2v_cbow_examples returns

@@ -31,7 +31,8 @@ __all__ = [
     "rdf2v_nonsink_starts", "rdf2v_random_walks", "rdf2v_random_walks_tokens",
     "rdf2v_unique_walks_workspace_size", "rdf2v_unique_walks", "rdf2v_bfs_walks_workspace_size",
     "rdf2v_bfs_walks", "rdf2v_skipgram_pairs_workspace_size",
-    "rdf2v_skipgram_pairs", "rdf2v_cbow_examples_workspace_size", "rdf2v_cbow_examples",
+    "rdf2v_skipgram_pairs", "rdf2v_skipgram_pairs_noalloc", "RDF2V_NOALLOC_MAX_WALKS",
+    "RDF2V_NOALLOC_SCRATCH_BYTES", "rdf2v_cbow_examples_workspace_size", "rdf2v_cbow_examples",
     "rdf2v_build_vocabulary_workspace_size", "rdf2v_build_vocabulary",
     "rdf2v_status_string", "check_device_status",
     "library_path",
@@ -53,6 +54,8 @@ RDF2V_MAX_DEPTH = 64
 RDF2V_TOKENS_TRIPLES = 0
 RDF2V_TOKENS_ENTITIES = 1
 RDF2V_TOKENS_PROPERTIES = 2
+RDF2V_NOALLOC_MAX_WALKS = 1 << 22
+RDF2V_NOALLOC_SCRATCH_BYTES = (32 << 20) + (64 << 10)
 
 _lib = None
 
@@ -105,6 +108,8 @@ def _native():
     lib.rdf2v_skipgram_pairs_workspace_size.restype = sz
     lib.rdf2v_skipgram_pairs.argtypes = [vp, vp, i64, i32, i32, vp, i64, vp, vp, sz, vp, vp]
     lib.rdf2v_skipgram_pairs.restype = ctypes.c_int
+    lib.rdf2v_skipgram_pairs_noalloc.argtypes = [vp, vp, i64, i32, i32, vp, i64, vp, vp, vp]
+    lib.rdf2v_skipgram_pairs_noalloc.restype = ctypes.c_int
     lib.rdf2v_cbow_examples_workspace_size.argtypes = [i64]
     lib.rdf2v_cbow_examples_workspace_size.restype = sz
     lib.rdf2v_cbow_examples.argtypes = [vp, vp, i64, i32, i32, vp, vp, i64, vp, vp, sz, vp, vp]
@@ -480,6 +485,30 @@ def rdf2v_skipgram_pairs(tokens: torch.Tensor, lens: torch.Tensor, window: int, 
         out = torch.empty((n, 2), dtype=torch.int32, device=dev)
         call(out, n)
         return out
+
+
+def rdf2v_skipgram_pairs_noalloc(tokens: torch.Tensor, lens: torch.Tensor, window: int, *, pairs: torch.Tensor,
+                                 count: torch.Tensor, status: torch.Tensor | None = None, stream=None):
+    """rdf2v_skipgram_pairs without a workspace, for callers that cannot allocate: the library's
+    fixed per-device scratch serves instead, so this binding allocates nothing either. The caller
+    supplies `pairs` [capacity, 2] and `count` (device int64 [1]); at most
+    RDF2V_NOALLOC_MAX_WALKS rows per call. Calls that overlap on one device race on the shared
+    scratch. Returns (pairs, count) without synchronising."""
+    _dev_i32(tokens, "tokens"); _dev_i32(lens, "lens")
+    dev = tokens.device
+    with _on_stream(dev, stream) as h:
+        w = int(lens.shape[0])
+        width = int(tokens.shape[1]) if tokens.dim() == 2 else 1
+        _same_device(dev, lens=lens)
+        if pairs.dim() != 2 or pairs.shape[1] != 2:
+            raise ValueError("pairs must have shape [capacity, 2]")
+        _out(pairs, "pairs", torch.int32, 0, dev)
+        _out(count, "count", torch.int64, 1, dev)
+        _status(status, dev)
+        st = _native().rdf2v_skipgram_pairs_noalloc(_ptr(tokens), _ptr(lens), w, width, window, _ptr(pairs),
+                                                    int(pairs.shape[0]), _ptr(count), _ptr(status), h)
+        _check(st, "rdf2v_skipgram_pairs_noalloc")
+        return pairs, count
 
 
 def rdf2v_cbow_examples_workspace_size(num_walks: int) -> int:

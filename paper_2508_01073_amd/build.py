@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "librdf2v.so")
 SOURCES = ["api.hip", "csr_build.hip", "random_walk.hip", "walk_edges.hip", "skipgram.hip", "unique_walks.hip", "bfs_walks.hip",
-           "vocab.hip"]
+           "vocab.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -69,6 +69,12 @@ int main(void) {
          RDF2V_ERR_TOO_LARGE);
   EXPECT(rdf2v_skipgram_pairs(FI, FI, 10, 0, 5, FI, 1, (int64_t *)F, F, 1 << 20, NULL, NULL) ==
          RDF2V_ERR_INVALID_ARGUMENT);
+  EXPECT(rdf2v_skipgram_pairs_noalloc(FI, FI, INT64_MAX, 9, 5, FI, 1, (int64_t *)F, NULL, NULL) ==
+         RDF2V_ERR_TOO_LARGE);
+  EXPECT(rdf2v_skipgram_pairs_noalloc(FI, FI, RDF2V_NOALLOC_MAX_WALKS + 1, 9, 5, FI, 1, (int64_t *)F, NULL, NULL) ==
+         RDF2V_ERR_TOO_LARGE);
+  EXPECT(rdf2v_skipgram_pairs_noalloc(FI, FI, 10, 0, 5, FI, 1, (int64_t *)F, NULL, NULL) ==
+         RDF2V_ERR_INVALID_ARGUMENT);
   EXPECT(rdf2v_cbow_examples(FI, FI, INT64_MAX, 129, 5, FI, FI, 1, (int64_t *)F, F, 1 << 20, NULL, NULL) ==
          RDF2V_ERR_TOO_LARGE);
   EXPECT(rdf2v_cbow_examples(FI, FI, 10, 9, 5, FI, FI, INT64_MAX, (int64_t *)F, F, 1 << 20, NULL, NULL) ==

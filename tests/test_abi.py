@@ -36,7 +36,7 @@ def test_header_declares_the_calls():
               "rdf2v_unique_walks", "rdf2v_unique_walks_workspace_size", "rdf2v_bfs_walks",
               "rdf2v_bfs_walks_workspace_size", "rdf2v_build_vocabulary",
               "rdf2v_build_vocabulary_workspace_size", "rdf2v_walk_edges_recommended",
-              "rdf2v_cbow_examples", "rdf2v_cbow_examples_workspace_size"]:
+              "rdf2v_cbow_examples", "rdf2v_cbow_examples_workspace_size", "rdf2v_skipgram_pairs_noalloc"]:
         assert n in names
 
 
@@ -200,6 +200,39 @@ def test_skipgram_argument_validation(lib):
     assert call(wsb=need - 1) == pkg.RDF2V_ERR_WORKSPACE
     assert pkg.rdf2v_skipgram_pairs_workspace_size(0) > 0
     assert pkg.rdf2v_skipgram_pairs_workspace_size(10**6) >= 8 * 10**6
+
+
+def test_skipgram_noalloc_argument_validation(lib):
+    # The same host-side checks as rdf2v_skipgram_pairs (no workspace to check), plus the fixed
+    # bound on rows per call; every rejection returns before any HIP call.
+    so, pkg = lib
+    f = so.rdf2v_skipgram_pairs_noalloc
+    E_INV = pkg.RDF2V_ERR_INVALID_ARGUMENT
+    ok_args = dict(tokens=FAKE, len=FAKE, n=100, width=9, window=5, pairs=FAKE8, cap=10, count=FAKE)
+
+    def call(**kw):
+        a = dict(ok_args, **kw)
+        return f(a["tokens"], a["len"], a["n"], a["width"], a["window"], a["pairs"], a["cap"], a["count"],
+                 None, None)
+
+    assert call(n=-1) == E_INV
+    assert call(window=-1) == E_INV
+    assert call(cap=-1) == E_INV
+    assert call(width=0) == E_INV
+    assert call(width=130) == E_INV
+    assert call(count=None) == E_INV
+    assert call(tokens=None) == E_INV
+    assert call(len=None) == E_INV
+    assert call(pairs=None) == E_INV
+    assert call(pairs=ctypes.c_void_p((1 << 40) + 4)) == E_INV
+    assert call(n=pkg.RDF2V_NOALLOC_MAX_WALKS + 1) == pkg.RDF2V_ERR_TOO_LARGE
+    assert call(n=1 << 40) == pkg.RDF2V_ERR_TOO_LARGE
+    # the library-held scratch holds the workspace of the largest call it takes
+    assert pkg.rdf2v_skipgram_pairs_workspace_size(pkg.RDF2V_NOALLOC_MAX_WALKS) <= pkg.RDF2V_NOALLOC_SCRATCH_BYTES
+    text = open(HEADER).read()
+    assert "#define RDF2V_NOALLOC_MAX_WALKS ((int64_t)1 << 22)" in text
+    assert "#define RDF2V_NOALLOC_SCRATCH_BYTES (((size_t)32 << 20) + ((size_t)64 << 10))" in text
+    assert pkg.RDF2V_NOALLOC_MAX_WALKS == 1 << 22 and pkg.RDF2V_NOALLOC_SCRATCH_BYTES == (32 << 20) + (64 << 10)
 
 
 def test_cbow_argument_validation(lib):
