@@ -8,6 +8,8 @@ checked for the at-any-size properties on the device and then compared
 bit-exactly with the oracle over all of its walks (the oracle runs on all
 host cores, over disjoint walk ranges; each ctypes call runs without the
 GIL), and windows across batch boundaries are recomputed by separate calls.
+Then all walks run in one call (13.2G output elements), compared with the oracle
+on windows past element 2^31, 2^32 and 2^33 and at the end.
 Takes a few minutes, most of it the oracle.
 """
 
@@ -71,3 +73,18 @@ def test_wikidata_share_batched_parity():
     say(f"[wikidata share] {num_walks} walks, {early / num_walks:.1%} stopped early, "
         f"{checked} rows compared bit-exact")
     assert 0.5 < early / num_walks < 0.99
+
+    # The whole corpus in one call: 13.2G output elements, so rows past element 2^31, 2^32 and
+    # 2^33 are written through the kernel's 64-bit row offsets; windows there and at the end are
+    # compared with the oracle, and the at-any-size properties hold for every row.
+    del tok_buf, len_buf, tok, ln
+    torch.cuda.empty_cache()
+    say("[wikidata share] all walks in one call")
+    tok1, ln1 = gpu_walks(csr, starts_dev, wpn, d, synth.WALK_SEED)
+    assert tok1.numel() > 2**33
+    rows = [(2**31 - 1) // width, 2**31 // width, 2**32 // width, 2**33 // width, num_walks - 1]
+    windows = [(max(0, min(r - 100, num_walks - 200)), 200) for r in rows]
+    compare_windows(csr, rp, ed, V, P, starts, wpn, d, synth.WALK_SEED, tok1, ln1, windows)
+    check_walk_properties(tok1, ln1, starts_dev, wpn, V, P, d)
+    say(f"[wikidata share] one call of {num_walks} walks: windows at elements 2^31, 2^32, 2^33 "
+        "and the end bit-exact")
