@@ -41,6 +41,21 @@ constexpr int kScanTile = kScanThreads * kScanItems;
 
 static_assert(kMaxBins <= kSortThreads, "one thread per digit in the tile prefix step");
 
+// Tile handled by workgroup b of a grid of `tiles` workgroups. Workgroups are
+// dealt to the 8 XCDs in turn (b mod 8), and each XCD has its own L2; this
+// mapping gives XCD x one contiguous range of tiles, which its workgroups
+// take in order. The runs that tiles t and t+1 write for one digit are
+// adjacent in the output and share a partially written cache line at their
+// boundary; with both tiles on one XCD the two halves of that line meet in
+// the same L2 instead of going to memory as two partial writes. A bijection
+// of [0, tiles), so the choice affects speed only.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t tiles) {
+  const int64_t x = b % kXcds, slot = b / kXcds;
+  const int64_t per = tiles / kXcds, rem = tiles % kXcds;
+  return x * per + min(x, rem) + slot;
+}
+
 // ---------------------------------------------------------------------------
 // Radix pass, step 1: per-tile digit histogram (+ id validation on pass 0).
 // ---------------------------------------------------------------------------
@@ -60,7 +75,7 @@ __global__ __launch_bounds__(kSortThreads) void radix_count_kernel(
   const int wave = threadIdx.x / kWave;
   for (int i = threadIdx.x; i < kTileWaves * kMaxBins; i += kSortThreads) (&hist[0][0])[i] = 0;
   __syncthreads();
-  const int64_t tile = blockIdx.x;
+  const int64_t tile = xcd_tile(blockIdx.x, tiles);
   const int64_t base = tile * kTile;
   const uintptr_t addr_bits = reinterpret_cast<uintptr_t>(keys) |
                               (kValidate ? (reinterpret_cast<uintptr_t>(pred) | reinterpret_cast<uintptr_t>(obj)) : 0);
@@ -141,7 +156,7 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
   const uint32_t mask = uint32_t(bins - 1);
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  const int64_t tile = blockIdx.x;
+  const int64_t tile = xcd_tile(blockIdx.x, tiles);
   const int64_t base = tile * kTile;
   const int tile_n = int(min(int64_t(kTile), n - base));
 
@@ -304,13 +319,39 @@ rdf2v_status scan_exclusive(int32_t *data, int64_t n, int32_t *partials, int64_t
 }
 
 // ---------------------------------------------------------------------------
-// row_ptr[v] = number of sorted subjects < v, for v in [0, V].
+// row_ptr[v] = number of sorted subjects < v, for v in [0, V], from the sorted
+// subjects in one pass: where the subject changes from a (at position i-1) to
+// b (at i), every v in (a, b] has row_ptr[v] = i; the subjects v above the
+// last one get n. A thread writes at most kGapRun of those entries; longer
+// runs of entities without out-edges keep the -1 that row_ptr_fill_kernel put
+// there, and row_ptr_fixup_kernel finds each of them by binary search.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void row_ptr_kernel(const uint32_t *__restrict__ sorted_keys,
-                                                      int64_t n, int32_t num_entities,
-                                                      int32_t *__restrict__ row_ptr) {
+constexpr int kGapRun = 64;
+
+__global__ __launch_bounds__(256) void row_ptr_fill_kernel(int32_t *__restrict__ row_ptr, int64_t nv) {
   const int64_t v = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (v > num_entities) return;
+  if (v < nv) row_ptr[v] = -1;
+}
+
+__global__ __launch_bounds__(256) void row_ptr_bounds_kernel(const uint32_t *__restrict__ sorted_keys,
+                                                             int64_t n, int32_t num_entities,
+                                                             int32_t *__restrict__ row_ptr) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (i > n) return;
+  // entities in (a, b] start at position i; a = -1 before the first subject, b = V after the last
+  const int64_t a = i == 0 ? -1 : int64_t(sorted_keys[i - 1]);
+  const int64_t b = i == n ? int64_t(num_entities) : int64_t(sorted_keys[i]);
+  if (b == a) return;
+  const int64_t hi = min(b, int64_t(num_entities));  // ids >= V cannot occur after validation
+  const int64_t lo = max(a + 1, hi - (kGapRun - 1));
+  for (int64_t v = lo; v <= hi; ++v) row_ptr[v] = int32_t(i);
+}
+
+__global__ __launch_bounds__(256) void row_ptr_fixup_kernel(const uint32_t *__restrict__ sorted_keys,
+                                                            int64_t n, int32_t num_entities,
+                                                            int32_t *__restrict__ row_ptr) {
+  const int64_t v = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (v > num_entities || row_ptr[v] >= 0) return;
   int64_t lo = 0, hi = n;
   while (lo < hi) {
     const int64_t mid = (lo + hi) >> 1;
@@ -439,8 +480,13 @@ rdf2v_status launch_csr_build(const int32_t *subj, const int32_t *pred, const in
     pay_in = pay_out;
   }
   const int64_t nv = int64_t(num_entities) + 1;
-  row_ptr_kernel<<<dim3(unsigned(ceil_div(nv, 256))), dim3(256), 0, stream>>>(keys_in, T, num_entities,
-                                                                              row_ptr_out);
+  row_ptr_fill_kernel<<<dim3(unsigned(ceil_div(nv, 256))), dim3(256), 0, stream>>>(row_ptr_out, nv);
+  RDF2V_LAUNCH_CHECK();
+  row_ptr_bounds_kernel<<<dim3(unsigned(ceil_div(T + 1, 256))), dim3(256), 0, stream>>>(keys_in, T, num_entities,
+                                                                                     row_ptr_out);
+  RDF2V_LAUNCH_CHECK();
+  row_ptr_fixup_kernel<<<dim3(unsigned(ceil_div(nv, 256))), dim3(256), 0, stream>>>(keys_in, T, num_entities,
+                                                                                   row_ptr_out);
   RDF2V_LAUNCH_CHECK();
   return RDF2V_OK;
 }
