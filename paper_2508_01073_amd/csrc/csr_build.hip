@@ -59,35 +59,40 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t tiles) {
 // ---------------------------------------------------------------------------
 // Radix pass, step 1: per-tile digit histogram (+ id validation on pass 0).
 // ---------------------------------------------------------------------------
-// Each thread reads kSortItems keys as 16-byte vectors (all loads issued
+// Each thread reads kCountItems keys as 16-byte vectors (all loads issued
 // before any histogram update) and counts them in its wave's own LDS
 // histogram, so lanes of different waves never contend for a bin.
+constexpr int kCountThreads = 256;
+constexpr int kCountWaves = kCountThreads / kWave;
+constexpr int kCountItems = kTile / kCountThreads;  // keys per thread
+
 template <bool kValidate>
-__global__ __launch_bounds__(kSortThreads) void radix_count_kernel(
+__global__ __launch_bounds__(kCountThreads) void radix_count_kernel(
     const uint32_t *__restrict__ keys, const int32_t *__restrict__ pred,
     const int32_t *__restrict__ obj, int64_t n, int shift, int bits, int32_t num_entities,
     int32_t num_predicates, int32_t *__restrict__ counts, int64_t tiles, int32_t *status) {
-  __shared__ int hist[kTileWaves][kMaxBins];
+  __shared__ int hist[kCountWaves * kMaxBins];
   constexpr int kVec = 4;
-  constexpr int kLoads = kSortItems / kVec;
+  constexpr int kLoads = kCountItems / kVec;
   const int bins = 1 << bits;
   const uint32_t mask = uint32_t(bins - 1);
   const int wave = threadIdx.x / kWave;
-  for (int i = threadIdx.x; i < kTileWaves * kMaxBins; i += kSortThreads) (&hist[0][0])[i] = 0;
+  for (int i = threadIdx.x; i < kCountWaves * bins; i += kCountThreads) hist[i] = 0;
   __syncthreads();
+  int *wave_hist = hist + wave * bins;
   const int64_t tile = xcd_tile(blockIdx.x, tiles);
   const int64_t base = tile * kTile;
   const uintptr_t addr_bits = reinterpret_cast<uintptr_t>(keys) |
                               (kValidate ? (reinterpret_cast<uintptr_t>(pred) | reinterpret_cast<uintptr_t>(obj)) : 0);
   const bool full = base + kTile <= n && (addr_bits & 15) == 0;
-  uint32_t k[kSortItems];
+  uint32_t k[kCountItems];
   int bad = 0;
   if (full) {
     // 16-byte loads: vector v of the tile holds keys 4v .. 4v+3.
     const uint4 *k4 = reinterpret_cast<const uint4 *>(keys + base);
 #pragma unroll
     for (int i = 0; i < kLoads; ++i) {
-      const uint4 v = k4[i * kSortThreads + threadIdx.x];
+      const uint4 v = k4[i * kCountThreads + threadIdx.x];
       k[kVec * i + 0] = v.x; k[kVec * i + 1] = v.y; k[kVec * i + 2] = v.z; k[kVec * i + 3] = v.w;
     }
     if (kValidate) {
@@ -95,26 +100,39 @@ __global__ __launch_bounds__(kSortThreads) void radix_count_kernel(
       const int4 *o4 = reinterpret_cast<const int4 *>(obj + base);
 #pragma unroll
       for (int i = 0; i < kLoads; ++i) {
-        const int4 pv = p4[i * kSortThreads + threadIdx.x];
-        const int4 ov = o4[i * kSortThreads + threadIdx.x];
+        const int4 pv = p4[i * kCountThreads + threadIdx.x];
+        const int4 ov = o4[i * kCountThreads + threadIdx.x];
         bad |= (uint32_t(pv.x) >= uint32_t(num_predicates)) | (uint32_t(pv.y) >= uint32_t(num_predicates)) |
                (uint32_t(pv.z) >= uint32_t(num_predicates)) | (uint32_t(pv.w) >= uint32_t(num_predicates));
         bad |= (uint32_t(ov.x) >= uint32_t(num_entities)) | (uint32_t(ov.y) >= uint32_t(num_entities)) |
                (uint32_t(ov.z) >= uint32_t(num_entities)) | (uint32_t(ov.w) >= uint32_t(num_entities));
       }
 #pragma unroll
-      for (int i = 0; i < kSortItems; ++i) bad |= k[i] >= uint32_t(num_entities);
+      for (int i = 0; i < kCountItems; ++i) bad |= k[i] >= uint32_t(num_entities);
     }
+    // After the first pass the keys of a tile are grouped by their lower digits, and in
+    // power-law graphs many tiles hold one hub's triples only: a wave's 64 increments of one
+    // bin would serialise on one LDS address. The lanes that share lane 0's digit add their
+    // number with one atomic instead.
+    const int lane = lane_id();
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) atomicAdd(&hist[wave][(k[i] >> shift) & mask], 1);
+    for (int i = 0; i < kCountItems; ++i) {
+      const uint32_t d = (k[i] >> shift) & mask;
+      const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
+      const uint64_t same = __ballot(d == d0);
+      if (d != d0)
+        atomicAdd(&wave_hist[d], 1);
+      else if (lane == 0)
+        atomicAdd(&wave_hist[d0], __popcll(same));
+    }
   } else {
     // ragged last tile or unaligned input: scalar loads of the same items
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
-      const int64_t idx = base + int64_t(i / kVec) * (kSortThreads * kVec) + threadIdx.x * kVec + (i % kVec);
+    for (int i = 0; i < kCountItems; ++i) {
+      const int64_t idx = base + int64_t(i / kVec) * (kCountThreads * kVec) + threadIdx.x * kVec + (i % kVec);
       if (idx < n) {
         const uint32_t key = keys[idx];
-        atomicAdd(&hist[wave][(key >> shift) & mask], 1);
+        atomicAdd(&wave_hist[(key >> shift) & mask], 1);
         if (kValidate) {
           bad |= key >= uint32_t(num_entities);
           bad |= uint32_t(obj[idx]) >= uint32_t(num_entities);
@@ -129,10 +147,10 @@ __global__ __launch_bounds__(kSortThreads) void radix_count_kernel(
   } else {
     __syncthreads();
   }
-  for (int d = threadIdx.x; d < bins; d += kSortThreads) {
+  for (int d = threadIdx.x; d < bins; d += kCountThreads) {
     int c = 0;
 #pragma unroll
-    for (int w = 0; w < kTileWaves; ++w) c += hist[w][d];
+    for (int w = 0; w < kCountWaves; ++w) c += hist[w * bins + d];
     counts[int64_t(d) * tiles + tile] = c;
   }
 }
@@ -333,18 +351,38 @@ __global__ __launch_bounds__(256) void row_ptr_fill_kernel(int32_t *__restrict__
   if (v < nv) row_ptr[v] = -1;
 }
 
+// Each thread takes kBoundItems consecutive positions (two 16-byte loads).
+constexpr int kBoundItems = 8;
+
 __global__ __launch_bounds__(256) void row_ptr_bounds_kernel(const uint32_t *__restrict__ sorted_keys,
                                                              int64_t n, int32_t num_entities,
                                                              int32_t *__restrict__ row_ptr) {
-  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (i > n) return;
+  const int64_t i0 = (int64_t(blockIdx.x) * 256 + threadIdx.x) * kBoundItems;
+  if (i0 > n) return;
+  uint32_t k[kBoundItems];
+  if (i0 + kBoundItems <= n && (reinterpret_cast<uintptr_t>(sorted_keys) & 15) == 0) {
+    const uint4 *k4 = reinterpret_cast<const uint4 *>(sorted_keys + i0);
+    const uint4 v0 = k4[0], v1 = k4[1];
+    k[0] = v0.x; k[1] = v0.y; k[2] = v0.z; k[3] = v0.w;
+    k[4] = v1.x; k[5] = v1.y; k[6] = v1.z; k[7] = v1.w;
+  } else {
+#pragma unroll
+    for (int j = 0; j < kBoundItems; ++j) k[j] = i0 + j < n ? sorted_keys[i0 + j] : 0u;
+  }
   // entities in (a, b] start at position i; a = -1 before the first subject, b = V after the last
-  const int64_t a = i == 0 ? -1 : int64_t(sorted_keys[i - 1]);
-  const int64_t b = i == n ? int64_t(num_entities) : int64_t(sorted_keys[i]);
-  if (b == a) return;
-  const int64_t hi = min(b, int64_t(num_entities));  // ids >= V cannot occur after validation
-  const int64_t lo = max(a + 1, hi - (kGapRun - 1));
-  for (int64_t v = lo; v <= hi; ++v) row_ptr[v] = int32_t(i);
+  int64_t a = i0 == 0 ? -1 : int64_t(sorted_keys[i0 - 1]);
+#pragma unroll
+  for (int j = 0; j < kBoundItems; ++j) {
+    const int64_t i = i0 + j;
+    if (i > n) break;
+    const int64_t b = i == n ? int64_t(num_entities) : int64_t(k[j]);
+    if (b != a) {
+      const int64_t hi = min(b, int64_t(num_entities));  // ids >= V cannot occur after validation
+      const int64_t lo = max(a + 1, hi - (kGapRun - 1));
+      for (int64_t v = lo; v <= hi; ++v) row_ptr[v] = int32_t(i);
+    }
+    a = b;
+  }
 }
 
 __global__ __launch_bounds__(256) void row_ptr_fixup_kernel(const uint32_t *__restrict__ sorted_keys,
@@ -457,11 +495,11 @@ rdf2v_status launch_csr_build(const int32_t *subj, const int32_t *pred, const in
     int2 *pay_out = ((plan.passes - 1 - pass) % 2 == 0) ? edges2 : pay_tmp;
     const dim3 grid(unsigned(plan.tiles));
     if (pass == 0)
-      radix_count_kernel<true><<<grid, dim3(kSortThreads), 0, stream>>>(
+      radix_count_kernel<true><<<grid, dim3(kCountThreads), 0, stream>>>(
           keys_in, pred, obj, T, shift, plan.digit_bits, num_entities, num_predicates, counts,
           plan.tiles, status_dev);
     else
-      radix_count_kernel<false><<<grid, dim3(kSortThreads), 0, stream>>>(
+      radix_count_kernel<false><<<grid, dim3(kCountThreads), 0, stream>>>(
           keys_in, nullptr, nullptr, T, shift, plan.digit_bits, num_entities, num_predicates,
           counts, plan.tiles, nullptr);
     RDF2V_LAUNCH_CHECK();
@@ -482,8 +520,8 @@ rdf2v_status launch_csr_build(const int32_t *subj, const int32_t *pred, const in
   const int64_t nv = int64_t(num_entities) + 1;
   row_ptr_fill_kernel<<<dim3(unsigned(ceil_div(nv, 256))), dim3(256), 0, stream>>>(row_ptr_out, nv);
   RDF2V_LAUNCH_CHECK();
-  row_ptr_bounds_kernel<<<dim3(unsigned(ceil_div(T + 1, 256))), dim3(256), 0, stream>>>(keys_in, T, num_entities,
-                                                                                     row_ptr_out);
+  row_ptr_bounds_kernel<<<dim3(unsigned(ceil_div(T + 1, 256 * kBoundItems))), dim3(256), 0, stream>>>(
+      keys_in, T, num_entities, row_ptr_out);
   RDF2V_LAUNCH_CHECK();
   row_ptr_fixup_kernel<<<dim3(unsigned(ceil_div(nv, 256))), dim3(256), 0, stream>>>(keys_in, T, num_entities,
                                                                                    row_ptr_out);
