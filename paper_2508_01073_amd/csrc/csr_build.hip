@@ -57,7 +57,9 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t tiles) {
 }
 
 // ---------------------------------------------------------------------------
-// Radix pass, step 1: per-tile digit histogram (+ id validation on pass 0).
+// Radix pass, step 1: per-tile digit histogram (+ subject id validation on
+// pass 0; the first scatter, which reads predicates and objects anyway,
+// validates those).
 // ---------------------------------------------------------------------------
 // Each thread reads kCountItems keys as 16-byte vectors (all loads issued
 // before any histogram update) and counts them in its wave's own LDS
@@ -68,9 +70,8 @@ constexpr int kCountItems = kTile / kCountThreads;  // keys per thread
 
 template <bool kValidate>
 __global__ __launch_bounds__(kCountThreads) void radix_count_kernel(
-    const uint32_t *__restrict__ keys, const int32_t *__restrict__ pred,
-    const int32_t *__restrict__ obj, int64_t n, int shift, int bits, int32_t num_entities,
-    int32_t num_predicates, int32_t *__restrict__ counts, int64_t tiles, int32_t *status) {
+    const uint32_t *__restrict__ keys, int64_t n, int shift, int bits, int32_t num_entities,
+    int32_t *__restrict__ counts, int64_t tiles, int32_t *status) {
   __shared__ int hist[kCountWaves * kMaxBins];
   constexpr int kVec = 4;
   constexpr int kLoads = kCountItems / kVec;
@@ -82,9 +83,7 @@ __global__ __launch_bounds__(kCountThreads) void radix_count_kernel(
   int *wave_hist = hist + wave * bins;
   const int64_t tile = xcd_tile(blockIdx.x, tiles);
   const int64_t base = tile * kTile;
-  const uintptr_t addr_bits = reinterpret_cast<uintptr_t>(keys) |
-                              (kValidate ? (reinterpret_cast<uintptr_t>(pred) | reinterpret_cast<uintptr_t>(obj)) : 0);
-  const bool full = base + kTile <= n && (addr_bits & 15) == 0;
+  const bool full = base + kTile <= n && (reinterpret_cast<uintptr_t>(keys) & 15) == 0;
   uint32_t k[kCountItems];
   int bad = 0;
   if (full) {
@@ -96,17 +95,6 @@ __global__ __launch_bounds__(kCountThreads) void radix_count_kernel(
       k[kVec * i + 0] = v.x; k[kVec * i + 1] = v.y; k[kVec * i + 2] = v.z; k[kVec * i + 3] = v.w;
     }
     if (kValidate) {
-      const int4 *p4 = reinterpret_cast<const int4 *>(pred + base);
-      const int4 *o4 = reinterpret_cast<const int4 *>(obj + base);
-#pragma unroll
-      for (int i = 0; i < kLoads; ++i) {
-        const int4 pv = p4[i * kCountThreads + threadIdx.x];
-        const int4 ov = o4[i * kCountThreads + threadIdx.x];
-        bad |= (uint32_t(pv.x) >= uint32_t(num_predicates)) | (uint32_t(pv.y) >= uint32_t(num_predicates)) |
-               (uint32_t(pv.z) >= uint32_t(num_predicates)) | (uint32_t(pv.w) >= uint32_t(num_predicates));
-        bad |= (uint32_t(ov.x) >= uint32_t(num_entities)) | (uint32_t(ov.y) >= uint32_t(num_entities)) |
-               (uint32_t(ov.z) >= uint32_t(num_entities)) | (uint32_t(ov.w) >= uint32_t(num_entities));
-      }
 #pragma unroll
       for (int i = 0; i < kCountItems; ++i) bad |= k[i] >= uint32_t(num_entities);
     }
@@ -133,11 +121,7 @@ __global__ __launch_bounds__(kCountThreads) void radix_count_kernel(
       if (idx < n) {
         const uint32_t key = keys[idx];
         atomicAdd(&wave_hist[(key >> shift) & mask], 1);
-        if (kValidate) {
-          bad |= key >= uint32_t(num_entities);
-          bad |= uint32_t(obj[idx]) >= uint32_t(num_entities);
-          bad |= uint32_t(pred[idx]) >= uint32_t(num_predicates);
-        }
+        if (kValidate) bad |= key >= uint32_t(num_entities);
       }
     }
   }
@@ -163,7 +147,8 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
     const uint32_t *__restrict__ keys_in, const int2 *__restrict__ pay_in,
     const int32_t *__restrict__ pred_in, const int32_t *__restrict__ obj_in,
     uint32_t *__restrict__ keys_out, int2 *__restrict__ pay_out, int64_t n, int shift, int bits,
-    const int32_t *__restrict__ offsets, int64_t tiles) {
+    const int32_t *__restrict__ offsets, int64_t tiles, int32_t num_entities, int32_t num_predicates,
+    int32_t *status) {
   __shared__ int wave_count[kTileWaves][kMaxBins];
   __shared__ int global_minus_local[kMaxBins];
   __shared__ uint32_t s_keys[kTile];
@@ -201,6 +186,13 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
       key[r] = keys_in[idx];
       pay[r] = kFirst ? make_int2(pred_in[idx], obj_in[idx]) : pay_in[idx];
     }
+  }
+  if (kFirst) {  // predicate and object ids (subjects were checked by the count pass)
+    int bad = 0;
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r)
+      bad |= (uint32_t(pay[r].x) >= uint32_t(num_predicates)) | (uint32_t(pay[r].y) >= uint32_t(num_entities));
+    if (__ballot(bad) != 0 && lane == 0 && status != nullptr) atomicOr(status, RDF2V_STATUS_ID_OUT_OF_RANGE);
   }
 #pragma unroll
   for (int r = 0; r < kRounds; ++r) {
@@ -453,7 +445,11 @@ SortPlan plan_csr_build(int64_t num_triples, int32_t num_entities) {
   // saves one pass in three but not one in four.
   p.passes = total_bits == 0 ? 1 : int(ceil_div(total_bits, 8));
   if (p.passes == 3 && total_bits <= 2 * kMaxDigitBits) p.passes = 2;
-  p.digit_bits = total_bits == 0 ? 1 : int(ceil_div(total_bits, p.passes));
+  // The bits are spread as evenly as the pass count allows, the first passes
+  // taking the odd ones: a pass of fewer bits has fewer bins and longer runs.
+  for (int k = 0; k < p.passes; ++k)
+    p.pass_bits[k] = total_bits == 0 ? 1 : total_bits / p.passes + (k < total_bits % p.passes ? 1 : 0);
+  p.digit_bits = p.pass_bits[0];
   p.tiles = ceil_div(num_triples, kTile);
   p.count_len = (int64_t(1) << p.digit_bits) * p.tiles;
   p.count_blocks = ceil_div(p.count_len, kScanTile);
@@ -488,34 +484,35 @@ rdf2v_status launch_csr_build(const int32_t *subj, const int32_t *pred, const in
 
   const uint32_t *keys_in = reinterpret_cast<const uint32_t *>(subj);
   const int2 *pay_in = nullptr;
+  int shift = 0;
   for (int pass = 0; pass < plan.passes; ++pass) {
-    const int shift = pass * plan.digit_bits;
+    const int bits = plan.pass_bits[pass];
+    const int64_t count_len = (int64_t(1) << bits) * plan.tiles;
     uint32_t *keys_out = (pass % 2 == 0) ? keys_a : keys_b;
     // The last pass must land in edges_out, so the payload alternates backwards from it.
     int2 *pay_out = ((plan.passes - 1 - pass) % 2 == 0) ? edges2 : pay_tmp;
     const dim3 grid(unsigned(plan.tiles));
     if (pass == 0)
       radix_count_kernel<true><<<grid, dim3(kCountThreads), 0, stream>>>(
-          keys_in, pred, obj, T, shift, plan.digit_bits, num_entities, num_predicates, counts,
-          plan.tiles, status_dev);
+          keys_in, T, shift, bits, num_entities, counts, plan.tiles, status_dev);
     else
       radix_count_kernel<false><<<grid, dim3(kCountThreads), 0, stream>>>(
-          keys_in, nullptr, nullptr, T, shift, plan.digit_bits, num_entities, num_predicates,
-          counts, plan.tiles, nullptr);
+          keys_in, T, shift, bits, num_entities, counts, plan.tiles, nullptr);
     RDF2V_LAUNCH_CHECK();
-    const rdf2v_status st = scan_exclusive(counts, plan.count_len, partials, plan.count_blocks, stream);
+    const rdf2v_status st = scan_exclusive(counts, count_len, partials, ceil_div(count_len, kScanTile), stream);
     if (st != RDF2V_OK) return st;
     if (pass == 0)
       radix_scatter_kernel<true><<<grid, dim3(kSortThreads), 0, stream>>>(
-          keys_in, nullptr, pred, obj, keys_out, pay_out, T, shift, plan.digit_bits, counts,
-          plan.tiles);
+          keys_in, nullptr, pred, obj, keys_out, pay_out, T, shift, bits, counts,
+          plan.tiles, num_entities, num_predicates, status_dev);
     else
       radix_scatter_kernel<false><<<grid, dim3(kSortThreads), 0, stream>>>(
-          keys_in, pay_in, nullptr, nullptr, keys_out, pay_out, T, shift, plan.digit_bits, counts,
-          plan.tiles);
+          keys_in, pay_in, nullptr, nullptr, keys_out, pay_out, T, shift, bits, counts,
+          plan.tiles, num_entities, num_predicates, nullptr);
     RDF2V_LAUNCH_CHECK();
     keys_in = keys_out;
     pay_in = pay_out;
+    shift += bits;
   }
   const int64_t nv = int64_t(num_entities) + 1;
   row_ptr_fill_kernel<<<dim3(unsigned(ceil_div(nv, 256))), dim3(256), 0, stream>>>(row_ptr_out, nv);

@@ -15,7 +15,8 @@ namespace rdf2v {
 // Layout of the rdf2v_build_csr workspace for (num_triples, num_entities).
 struct SortPlan {
   int passes = 0;      // LSD radix passes over the subject id
-  int digit_bits = 0;  // bits per pass (<= 8)
+  int digit_bits = 0;  // bits of the widest pass (<= 9); sizes the count table
+  int pass_bits[4] = {0, 0, 0, 0};  // bits of each pass, lowest digit first
   int64_t tiles = 0;   // 4096-triple tiles
   int64_t count_len = 0;     // digit-major count table length = bins * tiles
   int64_t count_blocks = 0;  // scan blocks over the count table
