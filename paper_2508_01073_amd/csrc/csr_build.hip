@@ -22,6 +22,7 @@
 
 #include "common.hpp"
 #include "launch.hpp"
+#include "xcd.hpp"
 
 namespace rdf2v {
 namespace {
@@ -40,21 +41,6 @@ constexpr int kScanItems = 16;
 constexpr int kScanTile = kScanThreads * kScanItems;
 
 static_assert(kMaxBins <= kSortThreads, "one thread per digit in the tile prefix step");
-
-// Tile handled by workgroup b of a grid of `tiles` workgroups. Workgroups are
-// dealt to the 8 XCDs in turn (b mod 8), and each XCD has its own L2; this
-// mapping gives XCD x one contiguous range of tiles, which its workgroups
-// take in order. The runs that tiles t and t+1 write for one digit are
-// adjacent in the output and share a partially written cache line at their
-// boundary; with both tiles on one XCD the two halves of that line meet in
-// the same L2 instead of going to memory as two partial writes. A bijection
-// of [0, tiles), so the choice affects speed only.
-constexpr int kXcds = 8;
-__device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t tiles) {
-  const int64_t x = b % kXcds, slot = b / kXcds;
-  const int64_t per = tiles / kXcds, rem = tiles % kXcds;
-  return x * per + min(x, rem) + slot;
-}
 
 // ---------------------------------------------------------------------------
 // Radix pass, step 1: per-tile digit histogram (+ subject id validation on
