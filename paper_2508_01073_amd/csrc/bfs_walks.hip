@@ -131,7 +131,6 @@ struct TinyTier {
   static constexpr int kCap = 384;
   static constexpr int kTreeCap = 96;
   static constexpr int kWavesPerSimd = 6;
-  static constexpr int kPerCu = 24;  // workgroups per CU (LDS-bound)
 };
 struct SmallTier {
   static constexpr int kThreads = 256;
