@@ -609,9 +609,11 @@ def rdf2v_build_vocabulary(subj, pred, obj, max_entities: int, max_predicates: i
         return ids[0], ids[1], ids[2], counts
 
 
-def check_device_status(status: torch.Tensor, where: str = "device") -> None:
-    """Raise if a device status word (zeroed before the calls) has any bit set."""
-    v = int(status.item())
+def check_device_status(status: torch.Tensor, where: str = "device", stream=None) -> None:
+    """Raise if a device status word (zeroed before the calls) has any bit set. The word is read
+    on `stream` (default: the current stream), so pass the stream the calls were made on."""
+    with _on_stream(status.device, stream):
+        v = int(status.item())
     if v != 0:
         bits = [n for b, n in [(RDF2V_STATUS_ID_OUT_OF_RANGE, "ID_OUT_OF_RANGE"),
                                (RDF2V_STATUS_BAD_CSR, "BAD_CSR"), (RDF2V_STATUS_BAD_LENGTH, "BAD_LENGTH"),

@@ -127,3 +127,12 @@ def test_calls_on_a_side_stream(graph):
         side.synchronize()
         assert torch.equal(pairs, pairs_ref)
         assert torch.equal(tok, tok_ref) and torch.equal(ln, ln_ref)
+    # a status word written on the side stream is read there: a bad start id queued behind
+    # long work must still be seen
+    st = torch.zeros(1, dtype=torch.int32, device=device())
+    side.wait_stream(torch.cuda.current_stream())
+    bad = torch.tensor([V + 5], dtype=torch.int32, device=device())
+    rd.rdf2v_random_walks(csr, starts, 4000, 8, 7, stream=side)
+    rd.rdf2v_random_walks(csr, bad, 1, 8, 7, status=st, stream=side)
+    with pytest.raises(rd.Rdf2vError):
+        rd.check_device_status(st, "side stream", stream=side)
