@@ -131,10 +131,16 @@ __device__ __forceinline__ uint64_t word7_of(uint32_t a0, uint32_t a1, uint32_t 
   return v & low_bytes_mask(r);
 }
 
-__device__ __forceinline__ uint64_t word7_lds(const uint32_t *lds, int32_t at, int64_t len, int i) {
+// Staged strings are at most kInlineBytes long, so their offsets and lengths fit 32 bits.
+__device__ __forceinline__ uint64_t word7_lds(const uint32_t *lds, int32_t at, int32_t len, int i) {
   const int32_t p = at + 7 * i;
   const int32_t a = p >> 2;
-  return word7_of(lds[a], lds[a + 1], lds[a + 2], uint32_t(p & 3) * 8, len - 7 * int64_t(i));
+  const int32_t r = len - 7 * i;
+  const uint64_t mask = r >= 7 ? kLow56 : (r <= 0 ? 0 : (uint64_t(1) << (8 * r)) - 1);
+  const uint32_t sh = uint32_t(p & 3) * 8;
+  const uint64_t lo = uint64_t(lds[a]) | (uint64_t(lds[a + 1]) << 32);
+  // (a2 << 31) << (33 - sh) is a2 << (64 - sh), and 0 for sh == 0.
+  return ((lo >> sh) | ((uint64_t(lds[a + 2]) << 31) << (33 - sh))) & mask;
 }
 
 __device__ __forceinline__ uint64_t word7_global(const StrCol *col, int64_t start, int64_t len, int64_t i) {
@@ -329,6 +335,7 @@ __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot
   constexpr int kStageLoads = (kPerCol - kPad + kBlock - 1) / kBlock;
   int64_t base[kCols];
   int32_t count[kCols];
+  int32_t nwhole[kCols];  // staged words that lie entirely inside the column
   uint32_t staged[kCols][kStageLoads];
 #pragma unroll
   for (int cc = 0; cc < kCols; ++cc) {
@@ -337,24 +344,26 @@ __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot
     base[cc] = ok ? (lo >> 2) : 0;
     const int64_t words = ok ? ((hi + 3) >> 2) - base[cc] : -1;
     count[cc] = (words >= 0 && words <= kPerCol - kPad) ? int32_t(words) : -1;
-    const uint32_t *src = reinterpret_cast<const uint32_t *>(seq.col[cc].chars);
     const int64_t whole = seq.col[cc].bytes >> 2;  // words that lie entirely inside the column
+    nwhole[cc] = count[cc] < 0 ? 0 : int32_t(min(int64_t(count[cc]), max(whole - base[cc], int64_t(0))));
+    const uint32_t *src = reinterpret_cast<const uint32_t *>(seq.col[cc].chars) + base[cc];
 #pragma unroll
     for (int j = 0; j < kStageLoads; ++j) {
       const int32_t i = tid + j * kBlock;
-      const int64_t g = base[cc] + i;
-      staged[cc][j] = (i < count[cc] && g < whole) ? src[g] : 0u;
+      staged[cc][j] = i < nwhole[cc] ? src[i] : 0u;
     }
   }
 #pragma unroll
   for (int cc = 0; cc < kCols; ++cc) {
     uint32_t *dst = stage + cc * kPerCol;
-    const int64_t whole = seq.col[cc].bytes >> 2;
 #pragma unroll
     for (int j = 0; j < kStageLoads; ++j) {
       const int32_t i = tid + j * kBlock;
-      if (i < count[cc]) dst[i] = base[cc] + i < whole ? staged[cc][j] : load_word(seq.col[cc], base[cc] + i);
+      if (i < nwhole[cc]) dst[i] = staged[cc][j];
     }
+    // A staged range that ends inside the column's last, partial word (at most one word) gets
+    // that word bytewise.
+    if (tid == 0 && nwhole[cc] < count[cc]) dst[nwhole[cc]] = load_word(seq.col[cc], base[cc] + nwhole[cc]);
     if (count[cc] >= 0 && tid < kPad) dst[count[cc] + tid] = 0;
   }
   __syncthreads();
