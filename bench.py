@@ -131,6 +131,7 @@ def _cpu_baseline(w, s, p, o, target_seconds: float, pinned_core, cores):
         "pinned_core": pinned_core,
         "nproc": len(cores),
         "cpu_model": cpu_model(),
+        "cpu_mhz": cpu_mhz(pinned_core),
     }
     # the all-core leg runs unpinned again (the caller restores the affinity set after this
     # function returns, so restore it here for the worker threads first)
@@ -158,6 +159,23 @@ def cpu_model() -> str:
     except OSError:
         pass
     return "unknown"
+
+
+def cpu_mhz(core: int | None) -> float | None:
+    """Current clock of a host core (MHz) as /proc/cpuinfo reports it, or None."""
+    try:
+        mhz = {}
+        proc = None
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("processor"):
+                proc = int(line.split(":", 1)[1])
+            elif line.startswith("cpu MHz") and proc is not None:
+                mhz[proc] = float(line.split(":", 1)[1])
+        if not mhz:
+            return None
+        return mhz.get(core, next(iter(mhz.values())))
+    except (OSError, ValueError):
+        return None
 
 
 def cpu_baseline_threads(oracle, rp, ed, V, P, starts, w, rate_1t: float, seconds: float, cores):
