@@ -230,13 +230,12 @@ __device__ __forceinline__ void stream_run(const int32_t *src, int32_t *dst, int
   for (int64_t q = head + 4 * body + t; q < total; q += kBlock) __builtin_nontemporal_store(src[q], dst + q);
 }
 
-// CBOW: one thread per (walk, position); walks_per_block = kBlock / width
-// walks per block, whose examples form one contiguous output range. With
-// kStage, the block copies its rows to LDS, places its centers and context rows
-// in LDS stages (at most kBlock examples, 2 * window ints per context row) and
-// streams each out as one contiguous run of 16-byte non-temporal stores;
-// otherwise each thread writes its own center and context row.
-template <bool kStage, int kBlock>
+// CBOW, staged: one thread per (walk, position); walks_per_block = kBlock / width
+// walks per block, whose examples form one contiguous output range. The block
+// copies its rows to LDS, places its centers and context rows in LDS stages
+// (at most kBlock examples, 2 * window ints per context row) and streams each
+// out as one contiguous run of 16-byte non-temporal stores.
+template <int kBlock>
 __global__ __launch_bounds__(kBlock) void cbow_emit_kernel(const int32_t *__restrict__ tokens,
                                                             const int32_t *__restrict__ len, int64_t n,
                                                             int32_t width, int32_t window,
@@ -244,9 +243,9 @@ __global__ __launch_bounds__(kBlock) void cbow_emit_kernel(const int32_t *__rest
                                                             int32_t *__restrict__ centers,
                                                             int32_t *__restrict__ contexts, int64_t capacity,
                                                             int32_t *status) {
-  extern __shared__ int32_t ctx_stage[];              // kStage: the block's context rows
-  __shared__ int32_t rows[kStage ? kBlock : 1];       // the block's walk rows
-  __shared__ int32_t ctr_stage[kStage ? kBlock : 1];  // kStage: the block's centers
+  extern __shared__ int32_t ctx_stage[];  // the block's context rows
+  __shared__ int32_t rows[kBlock];        // the block's walk rows
+  __shared__ int32_t ctr_stage[kBlock];   // the block's centers
   const int walks_per_block = kBlock / width;
   const int t = threadIdx.x;
   const int64_t r0 = int64_t(blockIdx.x) * walks_per_block;
@@ -266,43 +265,156 @@ __global__ __launch_bounds__(kBlock) void cbow_emit_kernel(const int32_t *__rest
     walk_first = offsets[r];
   }
   __shared__ int64_t block_end;
-  if (kStage) {
-    const int64_t span = (r_end - r0) * width;  // <= kBlock
-    if (t < span) rows[t] = tokens[r0 * width + t];
-    if (t == 0) {
-      if (r_end < n) {
-        block_end = offsets[r_end];
-      } else {
-        int b2 = 0;
-        block_end = offsets[n - 1] + clamped_len(len, n - 1, width, b2);
-      }
+  const int64_t span = (r_end - r0) * width;  // <= kBlock
+  if (t < span) rows[t] = tokens[r0 * width + t];
+  if (t == 0) {
+    if (r_end < n) {
+      block_end = offsets[r_end];
+    } else {
+      int b2 = 0;
+      block_end = offsets[n - 1] + clamped_len(len, n - 1, width, b2);
     }
-    __syncthreads();
   }
-  bool full = false;
+  __syncthreads();
   if (active && i < L) {
-    const int32_t *row = kStage ? rows + (t / width) * width : tokens + r * width;
+    const int32_t *row = rows + (t / width) * width;
     const int64_t e = walk_first + i;
-    if (e >= capacity) full = true;
-    if (kStage) ctr_stage[e - block_first] = row[i];
-    else if (e < capacity) centers[e] = row[i];
-    int32_t *ctx = kStage ? ctx_stage + (e - block_first) * cw : contexts + e * cw;
-    if (kStage || e < capacity) {
-      const int64_t j0 = max(int64_t(0), i - window), j1 = min(L - 1, i + int64_t(window));
-      int64_t m = 0;
-      for (int64_t j = j0; j <= j1; ++j)
-        if (j != i) ctx[m++] = row[j];
-      for (; m < cw; ++m) ctx[m] = -1;
+    ctr_stage[e - block_first] = row[i];
+    int32_t *ctx = ctx_stage + (e - block_first) * cw;
+    const int64_t j0 = max(int64_t(0), i - window), j1 = min(L - 1, i + int64_t(window));
+    int64_t m = 0;
+    for (int64_t j = j0; j <= j1; ++j)
+      if (j != i) ctx[m++] = row[j];
+    for (; m < cw; ++m) ctx[m] = -1;
+  }
+  __syncthreads();
+  // The block's examples end where the next block's begin.
+  const bool full = block_end > capacity;
+  const int64_t lim = max(int64_t(0), min(block_end, capacity) - block_first);  // examples that fit
+  stream_run<kBlock>(ctr_stage, centers + block_first, lim);
+  stream_run<kBlock>(ctx_stage, contexts + block_first * cw, lim * cw);
+  // `full` holds for the whole block: one thread reports it
+  if (((full && threadIdx.x == 0) || bad) && status != nullptr)
+    atomicOr(status, (full ? RDF2V_STATUS_CAPACITY : 0) | (bad ? RDF2V_STATUS_BAD_LENGTH : 0));
+}
+
+// CBOW, written in output order. A block of kBlock threads takes
+// kBlock / width walks, whose examples form one contiguous output range. It
+// stages only its walk rows and, per walk, where its examples start and how
+// many there are, plus the walk of each example; then every thread produces
+// context entries directly in output order, four per 16-byte non-temporal
+// store: entry m of example e is the m-th context of that example's position
+// (the tokens j0 .. j1 of its window, skipping the position itself), or -1
+// past the last one. No context row is ever staged, so the block's LDS does
+// not grow with the window.
+template <int kBlock>
+__global__ __launch_bounds__(kBlock) void cbow_direct_kernel(const int32_t *__restrict__ tokens,
+                                                              const int32_t *__restrict__ len, int64_t n,
+                                                              int32_t width, int32_t window,
+                                                              const int64_t *__restrict__ offsets,
+                                                              int32_t *__restrict__ centers,
+                                                              int32_t *__restrict__ contexts, int64_t capacity,
+                                                              int32_t *status) {
+  __shared__ int32_t rows[kBlock];        // the block's walk rows
+  __shared__ int32_t walk_first[kBlock];  // per walk of the block: its first example, block-relative
+  __shared__ int32_t walk_len[kBlock];    // per walk of the block: its examples (valid tokens)
+  __shared__ int32_t ex_walk[kBlock];     // per example of the block: its walk
+  __shared__ int64_t block_end;
+  const int walks_per_block = kBlock / width;
+  const int t = threadIdx.x;
+  const int64_t r0 = int64_t(blockIdx.x) * walks_per_block;
+  const int64_t r_end = min(n, r0 + walks_per_block);
+  const int k_walk = t / width;  // this thread's walk within the block
+  const int64_t r = r0 + k_walk;
+  const int i = t % width;
+  const bool active = t < walks_per_block * width && r < n;
+  int bad = 0;
+  // Every global read the block needs is issued before the first barrier.
+  const int64_t block_first = offsets[r0];
+  int32_t L = 0;
+  int64_t walk_first_g = 0;
+  if (active) {
+    L = clamped_len(len, r, width, bad);
+    walk_first_g = offsets[r];
+  }
+  const int64_t span = (r_end - r0) * width;  // <= kBlock
+  if (t < span) rows[t] = tokens[r0 * width + t];
+  if (t == 0) {
+    if (r_end < n) {
+      block_end = offsets[r_end];
+    } else {
+      int b2 = 0;
+      block_end = offsets[n - 1] + clamped_len(len, n - 1, width, b2);
     }
   }
-  if (kStage) {
-    __syncthreads();
-    // The block's examples end where the next block's begin.
-    const int64_t lim = max(int64_t(0), min(block_end, capacity) - block_first);  // examples that fit
-    stream_run<kBlock>(ctr_stage, centers + block_first, lim);
-    stream_run<kBlock>(ctx_stage, contexts + block_first * cw, lim * cw);
+  // Block-relative example indices: a block holds at most one example per thread.
+  const int32_t wf = int32_t(walk_first_g - block_first);
+  if (active && i == 0) {
+    walk_first[k_walk] = wf;
+    walk_len[k_walk] = L;
   }
-  if ((full || bad) && status != nullptr)
+  if (active && i < L) ex_walk[wf + i] = k_walk;
+  __syncthreads();
+
+  const int64_t cnt = block_end - block_first;                          // examples of the block
+  const int32_t lim = int32_t(max(int64_t(0), min(cnt, capacity - block_first)));  // those that fit
+  const bool full = block_end > capacity;
+  const int32_t w = window, cw = 2 * window;
+  // Centers: example e of the block is position e - walk_first of its walk.
+  for (int32_t e = t; e < lim; e += kBlock) {
+    const int32_t k = ex_walk[e];
+    __builtin_nontemporal_store(rows[k * width + (e - walk_first[k])], centers + block_first + e);
+  }
+  // Context entry q = e * cw + m of the block; `next` steps to entry q + 1.
+  struct Cursor {
+    int32_t e, m, base, nleft, nctx;  // example, entry; the example's window start, contexts before / in all
+  };
+  auto at = [&](int32_t e, int32_t m) {
+    Cursor c;
+    c.e = e;
+    c.m = m;
+    const int32_t k = ex_walk[e];
+    const int32_t pos = e - walk_first[k];
+    const int32_t j0 = max(0, pos - w), j1 = min(walk_len[k] - 1, pos + w);
+    c.base = k * width + j0;
+    c.nleft = pos - j0;
+    c.nctx = j1 - j0;
+    return c;
+  };
+  auto value = [&](const Cursor &c) {
+    return c.m < c.nleft ? rows[c.base + c.m] : (c.m < c.nctx ? rows[c.base + c.m + 1] : -1);
+  };
+  auto next = [&](Cursor &c) {
+    if (++c.m == cw && c.e + 1 < lim) c = at(c.e + 1, 0);
+  };
+  const int32_t total = lim * cw;  // entries that fit (<= kBlock * 2 * RDF2V_MAX_DEPTH * 2)
+  int32_t *dst = contexts + block_first * int64_t(cw);
+  const int32_t head = min(total, int32_t(((16 - (reinterpret_cast<uintptr_t>(dst) & 15)) & 15) / 4));
+  if (t < head) {
+    const Cursor c = at(t / cw, t % cw);
+    __builtin_nontemporal_store(value(c), dst + t);
+  }
+  const int32_t body = (total - head) >> 2;
+  v4i32 *dst4 = reinterpret_cast<v4i32 *>(dst + head);
+  for (int32_t q4 = t; q4 < body; q4 += kBlock) {
+    const int32_t q = head + 4 * q4;
+    Cursor c = at(q / cw, q % cw);
+    v4i32 v;
+    v.x = value(c);
+    next(c);
+    v.y = value(c);
+    next(c);
+    v.z = value(c);
+    next(c);
+    v.w = value(c);
+    __builtin_nontemporal_store(v, dst4 + q4);
+  }
+  for (int32_t q = head + 4 * body + t; q < total; q += kBlock) {
+    const Cursor c = at(q / cw, q % cw);
+    __builtin_nontemporal_store(value(c), dst + q);
+  }
+  // `full` holds for the whole block: one thread reports it
+  if (((full && threadIdx.x == 0) || bad) && status != nullptr)
     atomicOr(status, (full ? RDF2V_STATUS_CAPACITY : 0) | (bad ? RDF2V_STATUS_BAD_LENGTH : 0));
 }
 
@@ -389,10 +501,15 @@ rdf2v_status launch_cbow_examples(const int32_t *tokens, const int32_t *len, int
                                                                               partials, offsets);
   RDF2V_LAUNCH_CHECK();
   if (capacity == 0) return RDF2V_OK;
-  // A block of B threads holds at most B examples, so its stage is B rows of
-  // 2 * window ints: 256-thread blocks up to 32 KB, else 128 or 64, else direct
-  // stores. (Measured at window 5 on 48.9M walks: 512-thread blocks, or two or
-  // four positions per thread, were 2-50 % slower.)
+  // The staged kernel holds a block's context rows in LDS: B rows of
+  // 2 * window ints for B threads, 256-thread blocks up to 32 KB, else 128.
+  // The output-order kernel needs no stage. Measured on 8M walks of 17 tokens
+  // (ms, staged / output order): windows 1: 0.95 / 0.93, 2: 1.12 / 1.00,
+  // 5: 1.55 / 1.55, 10: 2.62 / 2.68, 20 (128 threads): 4.88 / 5.09, 40 (then
+  // 64-thread staged blocks): 14.2 / 9.1; so the staged kernel serves windows
+  // of 5 and more while a block of at least 128 threads holds its stage.
+  // (Earlier, at window 5 on 48.9M walks: 512-thread blocks, or two or four
+  // positions per thread, were 2-50 % slower.)
   const size_t row_bytes = size_t(2) * size_t(window) * sizeof(int32_t);
   auto launch = [&](auto kernel, int block, size_t lds) -> rdf2v_status {
     const int64_t blocks = ceil_div(num_walks, block / width);
@@ -402,13 +519,13 @@ rdf2v_status launch_cbow_examples(const int32_t *tokens, const int32_t *len, int
     RDF2V_LAUNCH_CHECK();
     return RDF2V_OK;
   };
-  if (width <= 256 && 256 * row_bytes <= kMaxStageBytes)
-    return launch(cbow_emit_kernel<true, 256>, 256, 256 * row_bytes);
-  if (width <= 128 && 128 * row_bytes <= kMaxStageBytes)
-    return launch(cbow_emit_kernel<true, 128>, 128, 128 * row_bytes);
-  if (width <= 64 && 64 * row_bytes <= kMaxStageBytes)
-    return launch(cbow_emit_kernel<true, 64>, 64, 64 * row_bytes);
-  return launch(cbow_emit_kernel<false, kThreads>, kThreads, 0);
+  if (window >= 5) {
+    if (width <= 256 && 256 * row_bytes <= kMaxStageBytes)
+      return launch(cbow_emit_kernel<256>, 256, 256 * row_bytes);
+    if (width <= 128 && 128 * row_bytes <= kMaxStageBytes)
+      return launch(cbow_emit_kernel<128>, 128, 128 * row_bytes);
+  }
+  return launch(cbow_direct_kernel<256>, 256, 0);
 }
 
 }  // namespace rdf2v
