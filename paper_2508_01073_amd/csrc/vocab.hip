@@ -10,14 +10,15 @@
 // inline copy of strings up to 98 bytes as 7-byte words, each with a
 // "written" byte on top, written by the claiming thread after its claim.
 //   1. insert_kernel (fast pass): a block stages the bytes of its strings in
-//      LDS with coalesced loads and hashes each string from there. For
-//      predicates, equal strings of the block are grouped first (exactly, in
-//      LDS) and only each group's first occurrence looks up the table. A
-//      lookup reads the key, minpos and the first inline word together, then
-//      the remaining words; equal tag and length plus equal inline words means
-//      the same string. A word not yet written leaves the occurrence to the
-//      general pass, as do strings that are not staged or too long to inline.
-//      No thread ever waits for another.
+//      LDS with coalesced loads and hashes each string from there, keeping its
+//      first eight 7-byte words in registers. For predicates, equal strings of
+//      the block are grouped first (exactly, in LDS) and only each group's
+//      first occurrence looks up the table. A lookup reads the key, minpos and
+//      the first eight inline words of a slot at once, with 16-byte loads (one
+//      round trip for strings up to 56 bytes); equal tag and length plus equal
+//      inline words means the same string. A word not yet written leaves the
+//      occurrence to the general pass, as do strings that are not staged or
+//      too long to inline. No thread ever waits for another.
 //   2. insert_general_kernel: the deferred occurrences, one thread each, from
 //      global memory; equal tags are settled against the representative's
 //      bytes whenever the inline copy does not decide.
@@ -34,6 +35,7 @@
 // wins a slot, only on minpos, so it is deterministic.
 
 #include <algorithm>
+#include <type_traits>
 
 #include "common.hpp"
 #include "launch.hpp"
@@ -122,8 +124,8 @@ __device__ __forceinline__ uint64_t low_bytes_mask(int64_t r) {  // the low min(
 }
 
 // Bytes [7i, 7i + 7) of a string as the low 56 bits of a word (zero past the
-// end). The LDS stage is padded with zero words, so its reads need no checks;
-// the global-memory form serves the general pass.
+// end), from global memory (the general pass) or from the LDS stage (the fast
+// pass; the stage is padded, so its reads need no checks).
 __device__ __forceinline__ uint64_t word7_of(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t sh, int64_t r) {
   const uint64_t lo = uint64_t(a0) | (uint64_t(a1) << 32);
   // (a2 << 31) << (33 - sh) is a2 << (64 - sh), and 0 for sh == 0.
@@ -131,16 +133,22 @@ __device__ __forceinline__ uint64_t word7_of(uint32_t a0, uint32_t a1, uint32_t 
   return v & low_bytes_mask(r);
 }
 
-// Staged strings are at most kInlineBytes long, so their offsets and lengths fit 32 bits.
+// Staged strings are at most kInlineBytes long, so their offsets and lengths
+// fit 32 bits. Each half of the word is one byte-aligned funnel shift of two
+// staged 4-byte words.
 __device__ __forceinline__ uint64_t word7_lds(const uint32_t *lds, int32_t at, int32_t len, int i) {
   const int32_t p = at + 7 * i;
   const int32_t a = p >> 2;
   const int32_t r = len - 7 * i;
-  const uint64_t mask = r >= 7 ? kLow56 : (r <= 0 ? 0 : (uint64_t(1) << (8 * r)) - 1);
-  const uint32_t sh = uint32_t(p & 3) * 8;
-  const uint64_t lo = uint64_t(lds[a]) | (uint64_t(lds[a + 1]) << 32);
-  // (a2 << 31) << (33 - sh) is a2 << (64 - sh), and 0 for sh == 0.
-  return ((lo >> sh) | ((uint64_t(lds[a + 2]) << 31) << (33 - sh))) & mask;
+  const uint32_t sh = uint32_t(p & 3);
+  const uint32_t x0 = lds[a], x1 = lds[a + 1], x2 = lds[a + 2];
+  uint32_t lo = __builtin_amdgcn_alignbyte(x1, x0, sh);                // bytes [p, p + 4)
+  uint32_t hi = __builtin_amdgcn_alignbyte(x2, x1, sh) & 0x00ffffffu;  // bytes [p + 4, p + 7)
+  if (r < 7) {
+    lo &= r >= 4 ? ~0u : (r <= 0 ? 0u : (1u << (8 * r)) - 1);
+    hi &= r <= 4 ? 0u : (1u << (8 * (r - 4))) - 1;
+  }
+  return (uint64_t(hi) << 32) | lo;
 }
 
 __device__ __forceinline__ uint64_t word7_global(const StrCol *col, int64_t start, int64_t len, int64_t i) {
@@ -172,105 +180,158 @@ __device__ __forceinline__ uint64_t load_u64(const uint64_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, kScope);
 }
 
-constexpr int kGroup = 1;           // inline words fetched together with the key
-constexpr int kBatchWords = 6;      // further inline words fetched together
-constexpr int32_t kDeferred = -2;   // parked in the id output: left to the general pass
+constexpr int32_t kDeferred = -2;  // parked in the id output: left to the general pass
+constexpr int kRegWords = 8;       // words of a string kept in registers and read with the key
+constexpr int kBatchPairs = 3;     // further pairs of inline words read together
 
-// The fast pass reads slots through the caches (wavefront-scope loads, which
-// may hit a line the CU's L1 or the XCD's L2 fetched earlier) instead of at
-// agent scope (loads marked device-coherent, which made the fast pass about
-// 20% slower on the 20M-triple power-law graph). A cached value can be
-// stale but never wrong, because every field moves one way during the pass:
-// the key goes from empty to its final value once (by compare-and-swap), each
-// inline word from 0 to its final value once, and minpos only decreases. So a
-// stale key reads as empty and the compare-and-swap then returns the real one;
-// a stale word reads as not written and the occurrence is left to the general
-// pass, which reads at agent scope; a stale minpos is larger than the real one
-// and at worst costs an atomicMin that changes nothing. Values left by earlier
-// kernels (a previous call on the same table) are not visible: each kernel
-// starts after the table was reset by the previous one.
-constexpr int kFastScope = __HIP_MEMORY_SCOPE_WAVEFRONT;
+// The fast pass reads slots with plain 16-byte loads (the key with minpos, and
+// pairs of inline words), which go through the caches and may hit a line the
+// CU's L1 or the XCD's L2 fetched earlier, rather than with device-coherent
+// loads (about 20% slower on the 20M-triple power-law graph), and with one
+// instruction per 16 bytes rather than one per field (the many-lines-per-wave
+// loads of the lookups are what the pass spends its time on). A value read
+// this way can be stale but never wrong, because every field moves one way
+// during the pass: the key goes from empty to its final value once (by
+// compare-and-swap), each inline word from 0 to its final value once, and
+// minpos only decreases. So a stale key reads as empty and the
+// compare-and-swap then returns the real one; a stale word reads as not
+// written and the occurrence is left to the general pass, which reads at agent
+// scope; a stale minpos is larger than the real one and at worst costs an
+// atomicMin that changes nothing. The checks also hold if a load were to see
+// one 4-byte half of a key or word updated and the other not: a key with
+// either half all ones goes through the compare-and-swap, and a word counts as
+// written only when its top byte says so and its low half is not zero (a word
+// whose low four bytes are zero is left to the general pass). Values left by
+// earlier kernels (a previous call on the same table) are not visible: each
+// kernel starts after the table was reset by the previous one.
+__device__ __forceinline__ uint4 load16(const void *p) { return *reinterpret_cast<const uint4 *>(p); }
+__device__ __forceinline__ uint64_t u64_of(uint32_t lo, uint32_t hi) { return uint64_t(lo) | (uint64_t(hi) << 32); }
 
-// What one look at a slot returns: the key, minpos and the first inline words,
-// all loaded at once (one round trip; they share the slot's line).
-struct SlotView {
-  uint64_t key;
-  int32_t minpos;
-  uint64_t w[kGroup];
-};
-
-__device__ __forceinline__ SlotView view_slot(const Slot *sl, int nw) {
-  SlotView v;
-  v.key = load_u64<kFastScope>(&sl->key);
-  v.minpos = __hip_atomic_load(&sl->minpos, __ATOMIC_RELAXED, kFastScope);
-#pragma unroll
-  for (int i = 0; i < kGroup; ++i) v.w[i] = i < nw ? load_u64<kFastScope>(&sl->words[i]) : 0;
-  return v;
+// A slot's inline word against the string's: 0 same, 1 different, 2 not written.
+__device__ __forceinline__ int word_state(uint64_t got, uint64_t want) {
+  if ((got & ~kLow56) != kWritten || uint32_t(got) == 0) return 2;
+  return got != (want | kWritten) ? 1 : 0;
 }
 
-// The table slot of one string (staged in LDS, at most kInlineBytes long) for
-// occurrence q: found, or claimed (then its inline copy is written), with minpos
-// lowered to q where needed. Returns the slot, kDeferred when an equal tag and
-// length meet an inline copy not yet fully written (the general pass settles
-// it), or -1 when the table is full.
+// The table slot of one string (staged in LDS, at most kInlineBytes long, its
+// first kRegWords words in wr) for occurrence q: found, or claimed (then its
+// inline copy is written), with minpos lowered to q where needed. Returns the
+// slot, kDeferred when an equal tag and length meet an inline copy not yet
+// fully written (the general pass settles it), or -1 when the table is full.
 __device__ __forceinline__ int32_t find_or_claim(Slot *__restrict__ table, int64_t mask, uint64_t h, int64_t q,
-                                                 const uint32_t *lds, int32_t at, int64_t len) {
+                                                 const uint32_t *lds, int32_t at, int64_t len,
+                                                 const uint64_t (&wr)[kRegWords]) {
   const int nw = int((len + 6) / 7);
   const uint64_t ident = ((h >> 44) << 12) | uint64_t(len);
   const uint64_t mine = (ident << 32) | uint32_t(q);
   int64_t s = int64_t(h & uint64_t(mask));
   for (int64_t probe = 0; probe <= mask; ++probe, s = (s + 1) & mask) {
     Slot *sl = table + s;
-    SlotView v = view_slot(sl, nw);
-    if (v.key == kEmpty) {
+    // One round trip: the key, minpos and the first kRegWords inline words.
+    const uint4 k4 = load16(&sl->key);
+    uint4 pr[kRegWords / 2];
+#pragma unroll
+    for (int j = 0; j < kRegWords / 2; ++j) pr[j] = 2 * j < nw ? load16(&sl->words[2 * j]) : make_uint4(0, 0, 0, 0);
+    uint64_t key = u64_of(k4.x, k4.y);
+    const int32_t minpos = int32_t(k4.z);
+    if (k4.x == 0xffffffffu || k4.y == 0xffffffffu) {  // empty, or seen while it changed
       const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long *>(&sl->key),
                                       static_cast<unsigned long long>(kEmpty),
                                       static_cast<unsigned long long>(mine));
       if (prev == kEmpty) {
-        for (int i = 0; i < nw; ++i)
+#pragma unroll
+        for (int i = 0; i < kRegWords; ++i)
+          if (i < nw) __hip_atomic_store(&sl->words[i], wr[i] | kWritten, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int i = kRegWords; i < nw; ++i)
           __hip_atomic_store(&sl->words[i], word7_lds(lds, at, len, i) | kWritten, __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
         atomicMin(&sl->minpos, int32_t(q));
         return int32_t(s);
       }
-      v.key = prev;
+      key = prev;
     }
-    if ((v.key >> 32) != ident) continue;
-    // Same tag and length: compare the inline copy (each word is written once,
-    // from 0, so a word is either not written yet or final).
-    bool unwritten = false, differ = false;
+    if ((key >> 32) != ident) continue;
+    // Same tag and length: compare the inline copy.
+    int seen = 0;  // bit k set: some word had state k
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i) {
-      if (i < nw) {
-        if ((v.w[i] & ~kLow56) != kWritten)
-          unwritten = true;
-        else if (v.w[i] != (word7_lds(lds, at, len, i) | kWritten))
-          differ = true;
-      }
+    for (int j = 0; j < kRegWords / 2; ++j) {
+      if (2 * j < nw) seen |= 1 << word_state(u64_of(pr[j].x, pr[j].y), wr[2 * j]);
+      if (2 * j + 1 < nw) seen |= 1 << word_state(u64_of(pr[j].z, pr[j].w), wr[2 * j + 1]);
     }
-    // The other words in batches whose loads are all in flight together.
+    // Longer strings: the other words in batches whose loads are all in flight together.
 #pragma unroll 1
-    for (int b = kGroup; b < nw; b += kBatchWords) {
-      uint64_t w[kBatchWords];
+    for (int b = kRegWords; b < nw; b += 2 * kBatchPairs) {
+      uint4 more[kBatchPairs];
 #pragma unroll
-      for (int j = 0; j < kBatchWords; ++j)
-        w[j] = b + j < nw ? load_u64<kFastScope>(&sl->words[b + j]) : 0;
+      for (int j = 0; j < kBatchPairs; ++j)
+        more[j] = b + 2 * j < nw ? load16(&sl->words[b + 2 * j]) : make_uint4(0, 0, 0, 0);
 #pragma unroll
-      for (int j = 0; j < kBatchWords; ++j) {
-        if (b + j < nw) {
-          if ((w[j] & ~kLow56) != kWritten)
-            unwritten = true;
-          else if (w[j] != (word7_lds(lds, at, len, b + j) | kWritten))
-            differ = true;
-        }
+      for (int j = 0; j < kBatchPairs; ++j) {
+        const int i = b + 2 * j;
+        if (i < nw) seen |= 1 << word_state(u64_of(more[j].x, more[j].y), word7_lds(lds, at, len, i));
+        if (i + 1 < nw) seen |= 1 << word_state(u64_of(more[j].z, more[j].w), word7_lds(lds, at, len, i + 1));
       }
     }
-    if (differ) continue;  // a different string
-    if (unwritten) return kDeferred;
-    if (int32_t(q) < v.minpos) atomicMin(&sl->minpos, int32_t(q));
+    if (seen & 2) continue;  // a different string
+    if (seen & 4) return kDeferred;
+    if (int32_t(q) < minpos) atomicMin(&sl->minpos, int32_t(q));
     return int32_t(s);
   }
   return -1;
+}
+
+// Copies the byte span [lo, hi) of each column (the block's strings of that
+// column) into its part of the LDS stage when it fits, and returns for each
+// column the first staged 4-byte word (base) and the number of staged words
+// (count), or count -1 when the span is not staged. Every load of every column
+// is issued before the first LDS store, so the stage costs one memory round
+// trip. With kWide (columns whose bytes start 16-byte aligned) the copy moves
+// 16-byte groups from a 16-byte aligned base, else 4-byte words; the group or
+// word holding a column's last bytes is rebuilt bytewise (nothing past a
+// column's end is read).
+template <int kCols, int kPerCol, int kPad, int kBlock, bool kWide>
+__device__ __forceinline__ void stage_spans(const Seq &seq, const int64_t (&span)[2][2], uint32_t *stage, int tid,
+                                            int64_t (&base)[kCols], int32_t (&count)[kCols]) {
+  constexpr int kUnit = kWide ? 4 : 1;  // words per load
+  constexpr int kUnits = kPerCol / kUnit;
+  constexpr int kLoads = (kUnits + kBlock - 1) / kBlock;
+  using Load = typename std::conditional<kWide, uint4, uint32_t>::type;
+  int32_t nunits[kCols], nwhole[kCols];  // staged units; those wholly inside the column
+  Load staged[kCols][kLoads];
+#pragma unroll
+  for (int cc = 0; cc < kCols; ++cc) {
+    const int64_t lo = span[cc][0], hi = span[cc][1];
+    const bool ok = lo >= 0 && lo <= hi && hi <= seq.col[cc].bytes;
+    base[cc] = ok ? ((lo >> 2) & ~int64_t(kUnit - 1)) : 0;
+    const int64_t words = ok ? ((hi + 3) >> 2) - base[cc] : -1;
+    count[cc] = (words >= 0 && words <= kPerCol - kPad) ? int32_t(words) : -1;
+    nunits[cc] = count[cc] < 0 ? 0 : (count[cc] + kUnit - 1) / kUnit;
+    const int64_t whole = (seq.col[cc].bytes >> 2) / kUnit - base[cc] / kUnit;
+    nwhole[cc] = int32_t(min(int64_t(nunits[cc]), max(whole, int64_t(0))));
+    const Load *src = reinterpret_cast<const Load *>(seq.col[cc].chars) + base[cc] / kUnit;
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      const int32_t u = tid + j * kBlock;
+      if constexpr (kWide)
+        staged[cc][j] = u < nwhole[cc] ? src[u] : make_uint4(0, 0, 0, 0);
+      else
+        staged[cc][j] = u < nwhole[cc] ? src[u] : 0u;
+    }
+  }
+#pragma unroll
+  for (int cc = 0; cc < kCols; ++cc) {
+    uint32_t *dst = stage + cc * kPerCol;
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      const int32_t u = tid + j * kBlock;
+      if (u < nwhole[cc]) reinterpret_cast<Load *>(dst)[u] = staged[cc][j];
+    }
+    if (tid == 0 && nwhole[cc] < nunits[cc]) {
+      for (int w = 0; w < kUnit; ++w)
+        dst[kUnit * nwhole[cc] + w] = load_word(seq.col[cc], base[cc] + kUnit * nwhole[cc] + w);
+    }
+    if (count[cc] >= 0 && tid < kPad) dst[count[cc] + tid] = 0;  // a zero tail for reads past the last string
+  }
 }
 
 // Fast pass. A block stages its strings in LDS and hashes them from there.
@@ -280,15 +341,15 @@ __device__ __forceinline__ int32_t find_or_claim(Slot *__restrict__ table, int64
 // are not hammered by every occurrence. Occurrences whose strings are not
 // staged or too long for an inline copy, and lookups that were deferred, are
 // parked as kDeferred for the general pass.
-template <bool kPaired, int kBlock, bool kGroupEqual>
+template <bool kPaired, int kBlock, bool kGroupEqual, bool kWide>
 __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot *__restrict__ table,
                                                         int64_t mask, int32_t *status) {
   constexpr int kCols = kPaired ? 2 : 1;
   constexpr int kWords = kBlock * kStageWordsPerString;
-  constexpr int kPerCol = kWords / kCols;  // includes kPad zero words
+  constexpr int kPerCol = kWords / kCols;  // includes kPad tail words
   constexpr int kPad = 4;
   constexpr int kLocal = 2 * kBlock;  // entries of the block's LDS table of distinct strings
-  __shared__ uint32_t stage[kWords];
+  __shared__ __align__(16) uint32_t stage[kWords];
   __shared__ int64_t span[2][2];  // per column: off[first row], off[last row + 1]
   // Grouping only (kGroupEqual):
   __shared__ uint64_t blk_hash[kGroupEqual ? kBlock : 1];
@@ -328,44 +389,9 @@ __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot
     len = b - a;
   }
   __syncthreads();
-  // Stage that span in LDS when it fits. Every load of every column is issued
-  // before the first LDS store, so the stage costs one memory round trip
-  // rather than one per kBlock words; words that reach past the column's last
-  // byte are rebuilt bytewise afterwards.
-  constexpr int kStageLoads = (kPerCol - kPad + kBlock - 1) / kBlock;
   int64_t base[kCols];
   int32_t count[kCols];
-  int32_t nwhole[kCols];  // staged words that lie entirely inside the column
-  uint32_t staged[kCols][kStageLoads];
-#pragma unroll
-  for (int cc = 0; cc < kCols; ++cc) {
-    const int64_t lo = span[cc][0], hi = span[cc][1];
-    const bool ok = lo >= 0 && lo <= hi && hi <= seq.col[cc].bytes;
-    base[cc] = ok ? (lo >> 2) : 0;
-    const int64_t words = ok ? ((hi + 3) >> 2) - base[cc] : -1;
-    count[cc] = (words >= 0 && words <= kPerCol - kPad) ? int32_t(words) : -1;
-    const int64_t whole = seq.col[cc].bytes >> 2;  // words that lie entirely inside the column
-    nwhole[cc] = count[cc] < 0 ? 0 : int32_t(min(int64_t(count[cc]), max(whole - base[cc], int64_t(0))));
-    const uint32_t *src = reinterpret_cast<const uint32_t *>(seq.col[cc].chars) + base[cc];
-#pragma unroll
-    for (int j = 0; j < kStageLoads; ++j) {
-      const int32_t i = tid + j * kBlock;
-      staged[cc][j] = i < nwhole[cc] ? src[i] : 0u;
-    }
-  }
-#pragma unroll
-  for (int cc = 0; cc < kCols; ++cc) {
-    uint32_t *dst = stage + cc * kPerCol;
-#pragma unroll
-    for (int j = 0; j < kStageLoads; ++j) {
-      const int32_t i = tid + j * kBlock;
-      if (i < nwhole[cc]) dst[i] = staged[cc][j];
-    }
-    // A staged range that ends inside the column's last, partial word (at most one word) gets
-    // that word bytewise.
-    if (tid == 0 && nwhole[cc] < count[cc]) dst[nwhole[cc]] = load_word(seq.col[cc], base[cc] + nwhole[cc]);
-    if (count[cc] >= 0 && tid < kPad) dst[count[cc] + tid] = 0;
-  }
+  stage_spans<kCols, kPerCol, kPad, kBlock, kWide>(seq, span, stage, tid, base, count);
   __syncthreads();
 
   const int64_t my_base = (kPaired && col == 1) ? base[kCols - 1] : base[0];
@@ -376,16 +402,23 @@ __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot
   const int32_t at = fast ? int32_t(start - 4 * my_base) : -1;
   const int nw = fast ? int((len + 6) / 7) : 0;
 
-  // Hash over the string's 7-byte words, which also form the inline copy.
+  // Hash over the string's 7-byte words, which also form the inline copy; the
+  // first kRegWords stay in registers for the lookup.
   uint64_t h = hash_seed(len);
+  uint64_t wr[kRegWords];
+#pragma unroll
+  for (int i = 0; i < kRegWords; ++i) {
+    wr[i] = i < nw ? word7_lds(lds, at, int32_t(len), i) : 0;
+    if (i < nw) h = hash_step(h, wr[i]);
+  }
 #pragma unroll 1
-  for (int i = 0; i < nw; ++i) h = hash_step(h, word7_lds(lds, at, len, i));
+  for (int i = kRegWords; i < nw; ++i) h = hash_step(h, word7_lds(lds, at, int32_t(len), i));
   h = fmix64(h);
 
   int32_t *out = ((kPaired && col == 1) ? seq.out[kCols - 1] : seq.out[0]) + seq_row<kPaired>(q);
   if constexpr (!kGroupEqual) {
     if (fast) {
-      const int32_t r = find_or_claim(table, mask, h, q, lds, at, len);
+      const int32_t r = find_or_claim(table, mask, h, q, lds, at, len, wr);
       if (r == -1 && status != nullptr) atomicOr(status, RDF2V_STATUS_CAPACITY);
       *out = r;
     } else if (active) {
@@ -411,7 +444,11 @@ __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot
             const uint32_t *olds = stage + seq_col<kPaired>(q0 + o) * kPerCol;
             const int32_t oat = blk_at[o];
             same = true;
-            for (int i = 0; i < nw && same; ++i) same = word7_lds(olds, oat, len, i) == word7_lds(lds, at, len, i);
+#pragma unroll
+            for (int i = 0; i < kRegWords; ++i)
+              if (i < nw) same = same && word7_lds(olds, oat, int32_t(len), i) == wr[i];
+            for (int i = kRegWords; i < nw && same; ++i)
+              same = word7_lds(olds, oat, int32_t(len), i) == word7_lds(lds, at, int32_t(len), i);
           }
         }
         if (same) {
@@ -423,7 +460,7 @@ __global__ __launch_bounds__(kBlock) void insert_kernel(Seq seq, int64_t n, Slot
     }
     __syncthreads();
     if (fast && loc_min[e] == tid) {
-      const int32_t r = find_or_claim(table, mask, h, q, lds, at, len);
+      const int32_t r = find_or_claim(table, mask, h, q, lds, at, len, wr);
       loc_slot[e] = r;
       if (r == -1 && status != nullptr) atomicOr(status, RDF2V_STATUS_CAPACITY);
     }
@@ -675,8 +712,15 @@ rdf2v_status run_seq(const Seq &seq, const SeqPlan &p, int64_t max_distinct, cha
     // Entities are mostly distinct within a block, predicates mostly repeated:
     // group equal strings only where that saves lookups.
     constexpr int kFastBlock = kPaired ? kFastBlockEntities : kFastBlockPredicates;
-    insert_kernel<kPaired, kFastBlock, !kPaired><<<dim3(unsigned(ceil_div(p.n, kFastBlock))), dim3(kFastBlock), 0,
-                                                   stream>>>(seq, p.n, table, p.capacity - 1, status);
+    const dim3 grid(unsigned(ceil_div(p.n, kFastBlock)));
+    bool wide = true;  // every column's bytes start 16-byte aligned
+    for (const StrCol &c : seq.col) wide = wide && (reinterpret_cast<uintptr_t>(c.chars) & 15) == 0;
+    if (wide)
+      insert_kernel<kPaired, kFastBlock, !kPaired, true><<<grid, dim3(kFastBlock), 0, stream>>>(seq, p.n, table,
+                                                                                             p.capacity - 1, status);
+    else
+      insert_kernel<kPaired, kFastBlock, !kPaired, false><<<grid, dim3(kFastBlock), 0, stream>>>(seq, p.n, table,
+                                                                                              p.capacity - 1, status);
     RDF2V_LAUNCH_CHECK();
     insert_general_kernel<kPaired><<<dim3(occ_blocks), dim3(kThreads), 0, stream>>>(seq, p.n, table,
                                                                                    p.capacity - 1, status);

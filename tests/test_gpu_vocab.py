@@ -27,27 +27,32 @@ def _column(strings, lead=0):
     return chars, off + lead
 
 
-def _dev_col(col):
+def _dev_col(col, shift=0):
+    """Device (chars, offsets); with `shift` the chars tensor is a view that starts
+    `shift` bytes into its allocation (4-byte aligned, as the ABI asks, but for
+    shift 4, 8, 12 not 16-byte aligned)."""
     chars, off = col
-    return (torch.from_numpy(np.ascontiguousarray(chars, np.uint8)).to(device()),
-            torch.from_numpy(np.ascontiguousarray(off, np.int64)).to(device()))
+    chars = np.ascontiguousarray(chars, np.uint8)
+    buf = torch.zeros(chars.size + shift, dtype=torch.uint8, device=device())
+    buf[shift:] = torch.from_numpy(chars).to(device())
+    return buf[shift:], torch.from_numpy(np.ascontiguousarray(off, np.int64)).to(device())
 
 
-def _run(cols, max_e, max_p, status=None, stream=None):
+def _run(cols, max_e, max_p, status=None, stream=None, shifts=(0, 0, 0)):
     st = new_status() if status is None else status
-    s, p, o, counts = rd.rdf2v_build_vocabulary(*[_dev_col(c) for c in cols], max_e, max_p, status=st,
-                                                stream=stream)
+    dcols = [_dev_col(c, k) for c, k in zip(cols, shifts)]
+    s, p, o, counts = rd.rdf2v_build_vocabulary(*dcols, max_e, max_p, status=st, stream=stream)
     torch.cuda.synchronize()
     return (s.cpu().numpy(), p.cpu().numpy(), o.cpu().numpy(), counts.cpu().numpy().tolist(),
             int(st.item()))
 
 
-def _compare(cols, what, max_e=None, max_p=None):
+def _compare(cols, what, max_e=None, max_p=None, shifts=(0, 0, 0)):
     ref = oracle.build_vocabulary(cols[0][0], cols[0][1], cols[1][0], cols[1][1], cols[2][0], cols[2][1])
     T = len(cols[0][1]) - 1
     max_e = max_e or max(1, 2 * T)
     max_p = max_p or max(1, T)
-    s, p, o, counts, flags = _run(cols, max_e, max_p)
+    s, p, o, counts, flags = _run(cols, max_e, max_p, shifts=shifts)
     assert flags == 0, f"{what}: status {flags}"
     assert counts == [ref[3], ref[4]], f"{what}: counts {counts} vs {ref[3:]}"
     for name, got, exp in (("subj", s, ref[0]), ("pred", p, ref[1]), ("obj", o, ref[2])):
@@ -93,6 +98,22 @@ def test_near_duplicates_every_alignment(seed):
     # bounds equal to the exact distinct counts are enough
     ref = oracle.build_vocabulary(cols[0][0], cols[0][1], cols[1][0], cols[1][1], cols[2][0], cols[2][1])
     _compare(cols, "exact bounds", max_e=ref[3], max_p=ref[4])
+
+
+@pytest.mark.parametrize("shifts", [(4, 4, 4), (0, 8, 0), (12, 0, 4)])
+def test_columns_not_16_byte_aligned(shifts):
+    # The fast pass stages 16-byte groups only when every column starts 16-byte
+    # aligned; these columns start 4 bytes past such a boundary (or 8, 12), in
+    # one column or all of them, so the 4-byte staging runs.
+    say(f"[vocab] column starts {shifts}")
+    rng = np.random.default_rng(11)
+    alphabet = [b"a", b"b", b"\x00", b"\xff"]
+    pool = [b"".join(rng.choice(alphabet, size=int(rng.integers(0, 12)))) for _ in range(300)]
+    pool += [b"http://kg.example.org/entity/Q" + str(k).encode() for k in range(300)]
+    T = 4000
+    cols = [_column([pool[i] for i in rng.integers(0, len(pool), T)], lead=int(rng.integers(0, 8)))
+            for _ in range(3)]
+    _compare(cols, f"column starts {shifts}", shifts=shifts)
 
 
 def test_inline_copy_length_boundary():
