@@ -61,6 +61,7 @@ struct alignas(128) Slot {
   uint64_t words[kInlineWords];  // inline copy: word i = bytes [7i, 7i + 7) | kWritten; 0 until written
 };
 static_assert(sizeof(Slot) == 128, "one slot per 128-byte line");
+static_assert(offsetof(Slot, minpos) == 8 && offsetof(Slot, words) == 16, "the slot layout the init kernel writes");
 
 struct StrCol {
   const uint8_t *chars;
@@ -558,20 +559,23 @@ __global__ __launch_bounds__(kThreads) void insert_general_kernel(Seq seq, int64
   if (bad && status != nullptr) atomicOr(status, RDF2V_STATUS_BAD_LENGTH);
 }
 
+// One 16-byte store per thread, each workgroup writing 4 KiB: the table as 16-byte groups (a
+// slot is eight of them; its first holds key, minpos and spare), then the bitset, two words per
+// thread.
 __global__ __launch_bounds__(kThreads) void init_kernel(Slot *__restrict__ table, int64_t capacity,
                                                         uint64_t *__restrict__ bits, int64_t words) {
-  const int64_t stride = int64_t(gridDim.x) * kThreads;
-  for (int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x; i < capacity || i < words; i += stride) {
-    if (i < capacity) {
-      Slot &sl = table[i];
-      sl.key = kEmpty;
-      sl.minpos = INT32_MAX;
-      sl.spare = 0;
-#pragma unroll
-      for (int k = 0; k < kInlineWords; ++k) sl.words[k] = 0;
-    }
-    if (i < words) bits[i] = 0;
+  constexpr int64_t kGroups = sizeof(Slot) / 16;
+  const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  const int64_t table_groups = capacity * kGroups;
+  if (i < table_groups) {
+    const uint4 v = (i % kGroups) == 0 ? make_uint4(0xffffffffu, 0xffffffffu, uint32_t(INT32_MAX), 0u)
+                                       : make_uint4(0u, 0u, 0u, 0u);
+    reinterpret_cast<uint4 *>(table)[i] = v;
+    return;
   }
+  const int64_t w = 2 * (i - table_groups);
+  if (w < words) bits[w] = 0;
+  if (w + 1 < words) bits[w + 1] = 0;
 }
 
 // Every used slot's minpos was lowered by the thread that claimed it, so it is
@@ -702,9 +706,9 @@ rdf2v_status run_seq(const Seq &seq, const SeqPlan &p, int64_t max_distinct, cha
   uint64_t *bits = reinterpret_cast<uint64_t *>(ws + p.bits_off);
   int32_t *prefix = reinterpret_cast<int32_t *>(ws + p.prefix_off);
   int64_t *partials = reinterpret_cast<int64_t *>(ws + p.partials_off);
-  const int64_t init_items = std::max(p.capacity, p.words);
-  const unsigned init_blocks = unsigned(std::min<int64_t>(ceil_div(init_items, kThreads), 8192));
-  init_kernel<<<dim3(init_blocks), dim3(kThreads), 0, stream>>>(table, p.capacity, bits, p.words);
+  const int64_t init_items = p.capacity * int64_t(sizeof(Slot) / 16) + ceil_div(p.words, 2);
+  init_kernel<<<dim3(unsigned(ceil_div(init_items, kThreads))), dim3(kThreads), 0, stream>>>(table, p.capacity,
+                                                                                            bits, p.words);
   RDF2V_LAUNCH_CHECK();
   const unsigned occ_blocks = unsigned(ceil_div(p.n, kThreads));
   const unsigned slot_blocks = unsigned(ceil_div(p.capacity, kThreads));
