@@ -25,11 +25,13 @@
 //   Either pass lowers minpos (read first, atomicMin only if smaller) and
 //   parks the slot index in the id output.
 //   3. mark_kernel: every used slot sets bit minpos of a bitset over the
-//      occurrences: the first occurrences of all strings.
+//      occurrences (the first occurrences of all strings) and writes minpos
+//      to a compact per-slot array.
 //   4. popcount scan: the rank of a first occurrence among all first
 //      occurrences is its id (int32 prefix per 64-bit word).
-//   5. slot_id_kernel writes the id of every used slot to a compact array;
-//      assign_kernel replaces the parked slot indices by ids.
+//   5. slot_id_kernel turns each used slot's first occurrence (left in a
+//      compact per-slot array by step 3) into its id; assign_kernel replaces
+//      the parked slot indices by ids.
 // The table is sized to a power of two >= 2 * the caller's bound on distinct
 // strings, so probing stays short; the result does not depend on which thread
 // wins a slot, only on minpos, so it is deterministic.
@@ -579,15 +581,19 @@ __global__ __launch_bounds__(kThreads) void init_kernel(Slot *__restrict__ table
 }
 
 // Every used slot's minpos was lowered by the thread that claimed it, so it is
-// an occurrence in [0, n); the range check only guards the bitset.
+// an occurrence in [0, n); the range check only guards the bitset. The slot's
+// first occurrence (or -1 for an unused slot) also goes to the compact id
+// array, so that slot_id_kernel reads 4 bytes per slot instead of the table.
 __global__ __launch_bounds__(kThreads) void mark_kernel(const Slot *__restrict__ table, int64_t capacity,
-                                                        int64_t n, unsigned long long *__restrict__ bits) {
+                                                        int64_t n, unsigned long long *__restrict__ bits,
+                                                        int32_t *__restrict__ ids) {
   const int64_t s = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   if (s >= capacity) return;
-  const uint64_t key = table[s].key;
-  const int32_t m = table[s].minpos;
-  if (key == kEmpty || m < 0 || m >= n) return;
-  atomicOr(bits + (m >> 6), 1ull << (m & 63));
+  const uint4 k4 = load16(&table[s].key);
+  const int32_t m = int32_t(k4.z);
+  const bool used = u64_of(k4.x, k4.y) != kEmpty && m >= 0 && m < n;
+  ids[s] = used ? m : -1;
+  if (used) atomicOr(bits + (m >> 6), 1ull << (m & 63));
 }
 
 __global__ __launch_bounds__(kThreads) void popc_count_kernel(const uint64_t *__restrict__ bits, int64_t words,
@@ -642,15 +648,15 @@ __global__ __launch_bounds__(kThreads) void word_prefix_kernel(const uint64_t *_
   }
 }
 
-__global__ __launch_bounds__(kThreads) void slot_id_kernel(const Slot *__restrict__ table, int64_t capacity,
-                                                           int64_t n, const uint64_t *__restrict__ bits,
+// The id of a used slot: the rank of its first occurrence among all first
+// occurrences (the compact array holds that occurrence, or -1).
+__global__ __launch_bounds__(kThreads) void slot_id_kernel(int64_t capacity, const uint64_t *__restrict__ bits,
                                                            const int32_t *__restrict__ prefix,
                                                            int32_t *__restrict__ ids) {
   const int64_t s = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   if (s >= capacity) return;
-  const uint64_t key = table[s].key;
-  const int32_t m = table[s].minpos;
-  if (key == kEmpty || m < 0 || m >= n) return;
+  const int32_t m = ids[s];
+  if (m < 0) return;
   const int64_t w = m >> 6;
   const uint64_t below = (uint64_t(1) << (m & 63)) - 1;
   ids[s] = prefix[w] + __popcll(bits[w] & below);
@@ -730,7 +736,7 @@ rdf2v_status run_seq(const Seq &seq, const SeqPlan &p, int64_t max_distinct, cha
                                                                                    p.capacity - 1, status);
     RDF2V_LAUNCH_CHECK();
     mark_kernel<<<dim3(slot_blocks), dim3(kThreads), 0, stream>>>(
-        table, p.capacity, p.n, reinterpret_cast<unsigned long long *>(bits));
+        table, p.capacity, p.n, reinterpret_cast<unsigned long long *>(bits), ids);
     RDF2V_LAUNCH_CHECK();
     popc_count_kernel<<<dim3(unsigned(p.blocks)), dim3(kThreads), 0, stream>>>(bits, p.words, partials);
     RDF2V_LAUNCH_CHECK();
@@ -741,7 +747,7 @@ rdf2v_status run_seq(const Seq &seq, const SeqPlan &p, int64_t max_distinct, cha
   if (p.n > 0) {
     word_prefix_kernel<<<dim3(unsigned(p.blocks)), dim3(kThreads), 0, stream>>>(bits, p.words, partials, prefix);
     RDF2V_LAUNCH_CHECK();
-    slot_id_kernel<<<dim3(slot_blocks), dim3(kThreads), 0, stream>>>(table, p.capacity, p.n, bits, prefix, ids);
+    slot_id_kernel<<<dim3(slot_blocks), dim3(kThreads), 0, stream>>>(p.capacity, bits, prefix, ids);
     RDF2V_LAUNCH_CHECK();
     assign_kernel<kPaired><<<dim3(occ_blocks), dim3(kThreads), 0, stream>>>(seq, p.n, ids);
     RDF2V_LAUNCH_CHECK();
